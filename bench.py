@@ -1,0 +1,232 @@
+"""Benchmark of the sparse INT8 linear path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c1]
+
+Workload (default): the DistilBERT FFN pair at batch 32 x seq 128 (M = 4096
+tokens), 4x1 block sparsity 90 %: W1 3072x768 (dequant + bias + GELU(erf) +
+requant to int8), W2 768x3072 (dequant + bias to fp32).
+
+One step is one pass of the whole hot path over one batch: quantize_act of the
+fp32 input -> linear 1 (int8 out) -> linear 2 (fp32 out), all on one stream.
+Inputs are resident in HBM when timing starts; the step rotates over enough
+input/output buffer sets (> 2x the 256 MB last-level cache) that every step
+reads its activations from HBM, not from a cache warmed by the previous step.
+
+Prints ONE JSON line. ``value`` is effective int8 TOPS over non-zero MACs
+(2 * M * 4 * stored_blocks per linear, summed) per step time. ``roofline``
+describes the slowest kernel of the step against the HBM bound, with its
+algorithmic bytes (X + Y + canonical packed W + scales) per launch divided by
+its average launch time from HIP events recorded around each launch.
+``cpu_baseline`` times the CPU oracle on the same step.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, published
+MFMA_I8_PEAK_TOPS = 5000.0   # MI355X dense int8 matrix peak, published
+MALL_BYTES = 256 << 20
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2211_07715_amd", "csrc", "kernels.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def kernel_source_hash() -> str:
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def algorithmic_bytes(m, n, k, nnzb, out_bytes):
+    """X + Y + canonical packed W (4 B values + 2 B column per block, row
+    pointers) + per-channel scale and bias."""
+    return m * k + m * n * out_bytes + nnzb * 6 + (n // 4 + 1) * 4 + 8 * n
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=200)
+    p.add_argument("--warmup", type=int, default=20)
+    p.add_argument("--workload", default="c1")
+    p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    p.add_argument("--cpu-seconds", type=float, default=10.0)
+    return p.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}), flush=True)
+        sys.exit(2)
+
+    import torch
+    import paper_2211_07715_amd as sl
+    import workloads as wk
+
+    sl.load()  # fails loudly without the HIP library
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}), flush=True)
+        sys.exit(2)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    wl = wk.workloads()[args.workload]
+    with open(os.path.join(ROOT, "tests", "golden", "calibration.json")) as f:
+        calib = json.load(f)[wl.name]
+    ops = wk.op_list(wl)
+    if wl.layers != 1:
+        raise SystemExit("bench workloads are single-layer op chains")
+
+    # ---- weights (packed once, offline)
+    packed, meta = [], []
+    for layer, op in ops:
+        key = f"L{layer}.{op.name}"
+        wd = wk.op_weight(wl, layer, op)
+        pw = sl.PackedWeight.pack(wd["w"], wd["sw"], wd["b"])
+        kind = sl.EPI_BY_NAME[wl.op_kind(layer, op)]
+        src = wl.op_src(layer, op)
+        meta.append(dict(key=key, n=op.n_out, k=op.k_in, kind=kind, src=src,
+                         so=float(calib.get(key, 1.0)), nnzb=pw.nnz_blocks(), stats=pw.tile_stats()))
+        packed.append(pw)
+    first = ops[0][1]
+    m = wl.m
+
+    # ---- activations: fp32 input whose quantisation is the seeded int8 X
+    sx = np.float32(wk.SX)
+    x_i8 = wk.op_seeded_x(wl, ops[0][0], first)
+    x_f32 = (x_i8.astype(np.float32) * sx).astype(np.float32)
+    out_bytes = {0: 4, 1: 4, 2: 4, 3: 1, 4: 1}
+    set_bytes = x_f32.nbytes + x_i8.nbytes + sum(m * md["n"] * out_bytes[md["kind"]] for md in meta)
+    n_sets = max(2, int(np.ceil(2.2 * MALL_BYTES / set_bytes)))
+    sets = []
+    xf_dev = torch.from_numpy(x_f32).to(dev)
+    for _ in range(n_sets):
+        s = {"xf": xf_dev.clone(), "q": torch.empty((m, first.k_in), dtype=torch.int8, device=dev)}
+        for md in meta:
+            dt = {0: torch.int32, 1: torch.float32, 2: torch.float32, 3: torch.int8, 4: torch.int8}[md["kind"]]
+            s[md["key"]] = torch.empty((m, md["n"]), dtype=dt, device=dev)
+        sets.append(s)
+    del xf_dev
+    stream = torch.cuda.current_stream()
+
+    def step(s, ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        sl.quantize_act(s["xf"], float(sx), out=s["q"], stream=stream)
+        if ev is not None:
+            ev[1].record(stream)
+        prev_key, prev_scale = None, float(sx)
+        for i, (pw, md) in enumerate(zip(packed, meta)):
+            if md["src"] == "seeded":
+                xin, xs = s["q"], float(sx)
+            else:
+                src = md["src"]
+                xin = s[src]
+                xs = next(mm["so"] for mm in meta if mm["key"] == src)
+            pw.run(xin, xs, md["kind"], out_scale=md["so"], out=s[md["key"]], stream=stream)
+            if ev is not None:
+                ev[2 + i].record(stream)
+
+    n_k = 1 + len(meta)
+    for i in range(args.warmup):
+        step(sets[i % n_sets])
+    torch.cuda.synchronize()
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(n_k + 1)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(sets[i % n_sets], events[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per_kernel_ms = np.zeros(n_k)
+    for ev in events:
+        for j in range(n_k):
+            per_kernel_ms[j] += ev[j].elapsed_time(ev[j + 1])
+    span_ms = events[0][0].elapsed_time(events[-1][-1])
+    ms_per_step = span_ms / args.steps
+    per_kernel_us = per_kernel_ms / args.steps * 1e3
+
+    # ---- metric
+    total_ops = sum(2 * m * 4 * md["nnzb"] for md in meta)
+    tops = total_ops / (ms_per_step * 1e-3) / 1e12
+    names = ["quantize_act"] + [md["key"] for md in meta]
+    kbytes = [x_f32.nbytes + x_i8.nbytes] + [algorithmic_bytes(m, md["n"], md["k"], md["nnzb"], out_bytes[md["kind"]])
+                                             for md in meta]
+    kops = [0] + [2 * m * 4 * md["nnzb"] for md in meta]
+    kernels = {}
+    for j in range(n_k):
+        kernels[names[j]] = {"us": round(float(per_kernel_us[j]), 3),
+                             "hbm_GBs": round(kbytes[j] / (per_kernel_us[j] * 1e-6) / 1e9, 1),
+                             "tops": round(kops[j] / (per_kernel_us[j] * 1e-6) / 1e12, 2)}
+    dom = int(np.argmax(per_kernel_us))
+    achieved = kbytes[dom] / (per_kernel_us[dom] * 1e-6) / 1e9
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        with open(TRAFFIC_FILE) as f:
+            tr = json.load(f)
+        if tr.get("kernel_source_sha256_16") == kernel_source_hash() and names[dom] in tr.get("kernels", {}):
+            traffic = tr["kernels"][names[dom]]["hbm_bytes_per_launch"]
+    roofline = {"bound": "hbm", "kernel": names[dom], "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                "algorithmic_bytes": int(kbytes[dom])}
+
+    # ---- CPU oracle baseline on the same step (bounded by time)
+    cpu = None
+    if not args.no_cpu:
+        import oracle
+        ws = [wk.op_weight(wl, layer, op) for layer, op in ops]
+        reps, t_cpu = 0, 0.0
+        while t_cpu < args.cpu_seconds and reps < 50:
+            c0 = time.perf_counter()
+            q = oracle.quantize(x_f32, sx)
+            outs = {}
+            for (layer, op), wd, md in zip(ops, ws, meta):
+                if md["src"] == "seeded":
+                    xin, xs = q, float(sx)
+                else:
+                    xin = outs[md["src"]]
+                    xs = next(mm["so"] for mm in meta if mm["key"] == md["src"])
+                outs[md["key"]] = oracle.linear(xin, wd["w"], xs, wd["sw"], wd["b"], md["kind"], so=md["so"])
+            t_cpu += time.perf_counter() - c0
+            reps += 1
+        cpu = {"value": round(total_ops * reps / t_cpu / 1e12, 5), "unit": "TOPS", "cores": oracle.threads(),
+               "kind": "oracle",
+               "sample": f"{reps} full step(s) of {wl.name} ({m} tokens; quantize + {len(meta)} linears, dense "
+                         f"naive int32 matmul), {t_cpu:.1f} s",
+               "ms_per_step": round(t_cpu / reps * 1e3, 1)}
+
+    line = {
+        "metric": "effective int8 TOPS (nonzero MACs) + % roofline; DistilBERT-layer latency @bs1/bs32",
+        "value": round(tops, 3),
+        "unit": "TOPS",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "i8",
+        "data": "synthetic",
+        "config": {"workload": f"{wl.name}: {wl.notes}", "m_tokens": m,
+                   "ops": [f"{md['key']} {md['n']}x{md['k']} kind={md['kind']} nnzb={md['nnzb']}" for md in meta],
+                   "buffer_sets": n_sets, "wall_s": round(wall, 3)},
+        "kernels": kernels,
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

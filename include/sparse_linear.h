@@ -108,7 +108,9 @@ sl_status sparse_linear_pack_host(const int8_t *w_host, int32_t n_out, int32_t k
  *   out_scale     per-tensor output scale, finite and > 0, for the int8 kinds
  *                 (ignored otherwise).
  *   y_dev         [m_tokens x n_out] device pointer of the kind's element type
- *                 (int32, fp32 or int8); must not overlap x_dev.
+ *                 (int32, fp32 or int8); must not overlap x_dev; 16-byte
+ *                 aligned for int32/fp32 output, 4-byte aligned for int8
+ *                 (else SL_ERR_INVALID_ARG).
  *   hip_stream    a hipStream_t (NULL = the legacy default stream).
  * The caller keeps X and Y alive until the stream has passed the call.
  */

@@ -43,7 +43,6 @@ def _load() -> ctypes.CDLL:
         if not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
             build()
         lib = ctypes.CDLL(LIB)
-        i8p = ctypes.POINTER(ctypes.c_int8)
         vp = ctypes.c_void_p
         lib.oracle_acc.argtypes = [vp, vp, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, vp]
         lib.oracle_acc.restype = None
@@ -59,7 +58,8 @@ def _load() -> ctypes.CDLL:
         lib.oracle_gelu.restype = ctypes.c_float
         lib.oracle_absmax_f32.argtypes = [vp, ctypes.c_int64]
         lib.oracle_absmax_f32.restype = ctypes.c_float
-        del i8p
+        lib.oracle_threads.argtypes = []
+        lib.oracle_threads.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -137,3 +137,8 @@ def absmax(v: np.ndarray) -> np.float32:
 def calibrate_out_scale(g: np.ndarray) -> np.float32:
     """Output scale so = max|g| / 127 (fp32), g the op's fp32 pre-requant output."""
     return np.float32(absmax(g) / np.float32(127.0))
+
+
+def threads() -> int:
+    """OpenMP threads the oracle's loops use."""
+    return int(_load().oracle_threads())

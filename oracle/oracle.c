@@ -21,6 +21,9 @@
 #include <math.h>
 #include <stdint.h>
 #include <stddef.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 
 enum {
     ORACLE_ACC_I32 = 0,  /* raw int32 accumulators                       */
@@ -154,4 +157,14 @@ float oracle_absmax_f32(const float *v, int64_t count)
         if (a > best) best = a;
     }
     return best;
+}
+
+/* Number of threads the OpenMP loops above use. */
+int oracle_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
 }

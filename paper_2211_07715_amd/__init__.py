@@ -1,0 +1,199 @@
+"""Python binding of the gfx950 sparse INT8 linear library (libsparse_linear.so).
+
+Argument marshalling only: every step of the layer runs in the library's HIP
+kernels. PyTorch is used for device memory and streams. There is no CPU or
+PyTorch fallback: if the shared library is missing, ``load()`` raises.
+
+    import paper_2211_07715_amd as sl
+    pw = sl.PackedWeight.pack(w_int8, w_scale, bias)        # host -> device, once
+    q = sl.quantize_act(x_f32_cuda, x_scale)                 # first op of a chain
+    y = pw.run(q, x_scale, sl.EPI_I8_GELU, out_scale=so)     # int8 [M, N]
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libsparse_linear.so")
+
+EPI_ACC_I32, EPI_F32, EPI_F32_GELU, EPI_I8, EPI_I8_GELU = 0, 1, 2, 3, 4
+EPI_BY_NAME = {"acc_i32": 0, "f32": 1, "f32_gelu": 2, "i8": 3, "i8_gelu": 4}
+
+SL_OK = 0
+STATUS = {0: "SL_OK", -1: "SL_ERR_INVALID_ARG", -2: "SL_ERR_SHAPE", -3: "SL_ERR_HIP", -4: "SL_ERR_OOM",
+          -5: "SL_ERR_UNSUPPORTED", -6: "SL_ERR_NOT_ON_DEVICE"}
+
+# every symbol include/sparse_linear.h declares
+EXPORTS = ("sparse_linear_pack", "sparse_linear_pack_host", "sparse_linear_run", "quantize_act",
+           "sparse_linear_unpack", "sparse_linear_info", "sparse_linear_export_bsr",
+           "sparse_linear_tile_stats", "sparse_linear_free", "sl_status_string", "sl_last_error",
+           "sl_abi_version")
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+class SparseLinearError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        super().__init__(f"{where}: {STATUS.get(status, status)}: {detail}")
+        self.status = status
+
+
+def load() -> ctypes.CDLL:
+    """Load the in-tree shared library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2211_07715_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64, f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float
+    pp = ctypes.POINTER(ctypes.c_void_p)
+    lib.sparse_linear_pack.argtypes = [vp, i32, i32, i32, i32, vp, vp, pp]
+    lib.sparse_linear_pack_host.argtypes = [vp, i32, i32, i32, i32, vp, vp, pp]
+    lib.sparse_linear_run.argtypes = [vp, vp, i64, f32, i32, f32, vp, vp]
+    lib.quantize_act.argtypes = [vp, i64, f32, vp, vp]
+    lib.sparse_linear_unpack.argtypes = [vp, vp]
+    lib.sparse_linear_info.argtypes = [vp, vp, vp, vp]
+    lib.sparse_linear_export_bsr.argtypes = [vp, vp, vp, vp]
+    lib.sparse_linear_tile_stats.argtypes = [vp, vp, vp, vp, vp]
+    for name in ("sparse_linear_pack", "sparse_linear_pack_host", "sparse_linear_run", "quantize_act",
+                 "sparse_linear_unpack", "sparse_linear_info", "sparse_linear_export_bsr",
+                 "sparse_linear_tile_stats"):
+        getattr(lib, name).restype = i32
+    lib.sparse_linear_free.argtypes = [vp]
+    lib.sparse_linear_free.restype = None
+    lib.sl_status_string.argtypes = [i32]
+    lib.sl_status_string.restype = ctypes.c_char_p
+    lib.sl_last_error.argtypes = []
+    lib.sl_last_error.restype = ctypes.c_char_p
+    lib.sl_abi_version.argtypes = []
+    lib.sl_abi_version.restype = i32
+    _lib = lib
+    return lib
+
+
+def _check(status: int, where: str):
+    if status != SL_OK:
+        detail = load().sl_last_error().decode(errors="replace")
+        raise SparseLinearError(status, where, detail)
+
+
+def _np_ptr(a: Optional[np.ndarray]):
+    return None if a is None else ctypes.c_void_p(a.ctypes.data)
+
+
+def _stream_ptr(stream) -> Optional[int]:
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+class PackedWeight:
+    """An immutable packed 4x1 block-sparse int8 weight (one C handle)."""
+
+    def __init__(self, handle: int, n_out: int, k_in: int, on_device: bool):
+        self._h = ctypes.c_void_p(handle)
+        self.n_out = n_out
+        self.k_in = k_in
+        self.on_device = on_device
+
+    @classmethod
+    def pack(cls, w: np.ndarray, w_scale: np.ndarray, bias: Optional[np.ndarray] = None,
+             host_only: bool = False) -> "PackedWeight":
+        lib = load()
+        w = np.ascontiguousarray(w, dtype=np.int8)
+        if w.ndim != 2:
+            raise ValueError("w must be [n_out, k_in]")
+        sw = np.ascontiguousarray(w_scale, dtype=np.float32)
+        b = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
+        n, k = w.shape
+        if sw.shape != (n,) or (b is not None and b.shape != (n,)):
+            raise ValueError("w_scale and bias must have shape [n_out]")
+        h = ctypes.c_void_p()
+        fn = lib.sparse_linear_pack_host if host_only else lib.sparse_linear_pack
+        _check(fn(_np_ptr(w), n, k, 4, 1, _np_ptr(sw), _np_ptr(b), ctypes.byref(h)), fn.__name__)
+        return cls(h.value, n, k, not host_only)
+
+    @property
+    def handle(self) -> ctypes.c_void_p:
+        if not self._h:
+            raise ValueError("packed weight was freed")
+        return self._h
+
+    def free(self):
+        if self._h:
+            load().sparse_linear_free(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+    def info(self):
+        n, k, nnzb = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int64()
+        _check(load().sparse_linear_info(self.handle, ctypes.byref(n), ctypes.byref(k), ctypes.byref(nnzb)),
+               "sparse_linear_info")
+        return n.value, k.value, nnzb.value
+
+    def nnz_blocks(self) -> int:
+        return self.info()[2]
+
+    def unpack(self) -> np.ndarray:
+        out = np.empty((self.n_out, self.k_in), dtype=np.int8)
+        _check(load().sparse_linear_unpack(self.handle, _np_ptr(out)), "sparse_linear_unpack")
+        return out
+
+    def export_bsr(self):
+        nnzb = self.nnz_blocks()
+        row_ptr = np.empty(self.n_out // 4 + 1, dtype=np.uint32)
+        col = np.empty(nnzb, dtype=np.uint16)
+        vals = np.empty((nnzb, 4), dtype=np.int8)
+        _check(load().sparse_linear_export_bsr(self.handle, _np_ptr(row_ptr), _np_ptr(col), _np_ptr(vals)),
+               "sparse_linear_export_bsr")
+        return row_ptr, col, vals
+
+    def tile_stats(self):
+        nt, uc, pc, ib = ctypes.c_int32(), ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+        _check(load().sparse_linear_tile_stats(self.handle, ctypes.byref(nt), ctypes.byref(uc), ctypes.byref(pc),
+                                               ctypes.byref(ib)), "sparse_linear_tile_stats")
+        return {"n_tiles": nt.value, "union_cols": uc.value, "padded_cols": pc.value, "image_bytes": ib.value}
+
+    def run(self, x, x_scale: float, kind: int, out_scale: float = 1.0, out=None, stream=None):
+        """Y = epilogue(X W^T) for a CUDA int8 tensor x [M, k_in]; returns Y."""
+        import torch
+        if x.dtype != torch.int8 or x.dim() != 2 or x.shape[1] != self.k_in or not x.is_cuda:
+            raise ValueError(f"x must be a CUDA int8 tensor [M, {self.k_in}]")
+        if not x.is_contiguous():
+            raise ValueError("x must be contiguous")
+        dt = {EPI_ACC_I32: torch.int32, EPI_F32: torch.float32, EPI_F32_GELU: torch.float32,
+              EPI_I8: torch.int8, EPI_I8_GELU: torch.int8}[kind]
+        m = x.shape[0]
+        if out is None:
+            out = torch.empty((m, self.n_out), dtype=dt, device=x.device)
+        elif out.dtype != dt or tuple(out.shape) != (m, self.n_out) or not out.is_contiguous():
+            raise ValueError("out has the wrong dtype/shape or is not contiguous")
+        _check(load().sparse_linear_run(self.handle, ctypes.c_void_p(x.data_ptr()), m, float(x_scale), int(kind),
+                                        float(out_scale), ctypes.c_void_p(out.data_ptr()), _stream_ptr(stream)),
+               "sparse_linear_run")
+        return out
+
+
+def quantize_act(x, scale: float, out=None, stream=None):
+    """q = clamp(rint(x / scale), -127, 127) for a contiguous CUDA fp32 tensor."""
+    import torch
+    if x.dtype != torch.float32 or not x.is_cuda or not x.is_contiguous():
+        raise ValueError("x must be a contiguous CUDA float32 tensor")
+    if out is None:
+        out = torch.empty(x.shape, dtype=torch.int8, device=x.device)
+    elif out.dtype != torch.int8 or out.numel() != x.numel() or not out.is_contiguous():
+        raise ValueError("out must be a contiguous int8 tensor with x's size")
+    _check(load().quantize_act(ctypes.c_void_p(x.data_ptr()), x.numel(), float(scale),
+                               ctypes.c_void_p(out.data_ptr()), _stream_ptr(stream)), "quantize_act")
+    return out

@@ -1,0 +1,219 @@
+// C-ABI layer of the sparse INT8 linear library: argument checks, handle
+// lifetime and dispatch to the gfx950 kernels. No exception crosses the ABI.
+#include <math.h>
+#include <string.h>
+
+#include <new>
+#include <string>
+
+#include "sl_internal.h"
+
+namespace sl {
+
+static thread_local std::string g_last_error;
+
+void set_error(const std::string &msg) { g_last_error = msg; }
+void clear_error() { g_last_error.clear(); }
+
+}  // namespace sl
+
+using namespace sl;
+
+static sl_status pack_common(const int8_t *w_host, int32_t n_out, int32_t k_in, int32_t block_h,
+                             int32_t block_w, const float *w_scale_host, const float *bias_host,
+                             sl_packed_weight **out, bool upload)
+{
+    clear_error();
+    if (!out) {
+        set_error("out must not be NULL");
+        return SL_ERR_INVALID_ARG;
+    }
+    *out = nullptr;
+    sl_status st = validate_weight_args(w_host, n_out, k_in, block_h, block_w, w_scale_host, bias_host);
+    if (st != SL_OK) return st;
+    int device = -1;
+    if (upload) {
+        st = check_device_arch(&device);
+        if (st != SL_OK) return st;
+    }
+    sl_packed_weight *p = new (std::nothrow) sl_packed_weight();
+    if (!p) {
+        set_error("host allocation failed");
+        return SL_ERR_OOM;
+    }
+    st = build_host_image(w_host, n_out, k_in, w_scale_host, bias_host, p);
+    if (st == SL_OK && upload) {
+        p->dev.device = device;
+        st = upload_image(p);
+    }
+    if (st != SL_OK) {
+        sparse_linear_free(p);
+        return st;
+    }
+    *out = p;
+    return SL_OK;
+}
+
+extern "C" {
+
+sl_status sparse_linear_pack(const int8_t *w_host, int32_t n_out, int32_t k_in, int32_t block_h,
+                             int32_t block_w, const float *w_scale_host, const float *bias_host,
+                             sl_packed_weight **out)
+{
+    return pack_common(w_host, n_out, k_in, block_h, block_w, w_scale_host, bias_host, out, true);
+}
+
+sl_status sparse_linear_pack_host(const int8_t *w_host, int32_t n_out, int32_t k_in, int32_t block_h,
+                                  int32_t block_w, const float *w_scale_host, const float *bias_host,
+                                  sl_packed_weight **out)
+{
+    return pack_common(w_host, n_out, k_in, block_h, block_w, w_scale_host, bias_host, out, false);
+}
+
+static bool good_scale(float s) { return isfinite(s) && s > 0.0f; }
+
+sl_status sparse_linear_run(const sl_packed_weight *w, const int8_t *x_dev, int64_t m_tokens,
+                            float x_scale, int32_t epilogue_kind, float out_scale, void *y_dev,
+                            void *hip_stream)
+{
+    clear_error();
+    if (!w) {
+        set_error("w must not be NULL");
+        return SL_ERR_INVALID_ARG;
+    }
+    if (!w->on_device) {
+        set_error("handle was packed with sparse_linear_pack_host; pack it on a device to run");
+        return SL_ERR_NOT_ON_DEVICE;
+    }
+    if (epilogue_kind < SL_EPI_ACC_I32 || epilogue_kind > SL_EPI_I8_GELU) {
+        set_error("unknown epilogue kind " + std::to_string(epilogue_kind));
+        return SL_ERR_INVALID_ARG;
+    }
+    if (m_tokens < 0) {
+        set_error("m_tokens must be >= 0");
+        return SL_ERR_SHAPE;
+    }
+    if (epilogue_kind != SL_EPI_ACC_I32 && !good_scale(x_scale)) {
+        set_error("x_scale must be finite and > 0");
+        return SL_ERR_INVALID_ARG;
+    }
+    const bool i8 = epilogue_kind == SL_EPI_I8 || epilogue_kind == SL_EPI_I8_GELU;
+    if (i8 && !good_scale(out_scale)) {
+        set_error("out_scale must be finite and > 0 for the int8 epilogues");
+        return SL_ERR_INVALID_ARG;
+    }
+    if (m_tokens == 0) return SL_OK;
+    if (!x_dev || !y_dev) {
+        set_error("x_dev and y_dev must not be NULL");
+        return SL_ERR_INVALID_ARG;
+    }
+    const uintptr_t need = i8 ? 4 : 16;
+    if (reinterpret_cast<uintptr_t>(y_dev) % need) {
+        set_error("y_dev must be " + std::to_string(need) + "-byte aligned for this epilogue");
+        return SL_ERR_INVALID_ARG;
+    }
+    // fl(1/so), one fp32 division, as the definition states
+    const float inv_so = i8 ? 1.0f / out_scale : 1.0f;
+    return launch_linear(w, x_dev, m_tokens, x_scale, epilogue_kind, inv_so, y_dev, hip_stream);
+}
+
+sl_status quantize_act(const float *x_dev, int64_t numel, float scale, int8_t *q_dev, void *hip_stream)
+{
+    clear_error();
+    if (numel < 0) {
+        set_error("numel must be >= 0");
+        return SL_ERR_SHAPE;
+    }
+    if (!good_scale(scale)) {
+        set_error("scale must be finite and > 0");
+        return SL_ERR_INVALID_ARG;
+    }
+    if (numel == 0) return SL_OK;
+    if (!x_dev || !q_dev) {
+        set_error("x_dev and q_dev must not be NULL");
+        return SL_ERR_INVALID_ARG;
+    }
+    const float inv = 1.0f / scale;
+    return launch_quantize(x_dev, numel, inv, q_dev, hip_stream);
+}
+
+sl_status sparse_linear_unpack(const sl_packed_weight *w, int8_t *w_host)
+{
+    clear_error();
+    if (!w || !w_host) {
+        set_error("w and w_host must not be NULL");
+        return SL_ERR_INVALID_ARG;
+    }
+    return decode_tile_image(w, w_host);
+}
+
+sl_status sparse_linear_info(const sl_packed_weight *w, int32_t *n_out, int32_t *k_in, int64_t *nnz_blocks)
+{
+    clear_error();
+    if (!w) {
+        set_error("w must not be NULL");
+        return SL_ERR_INVALID_ARG;
+    }
+    if (n_out) *n_out = w->n_out;
+    if (k_in) *k_in = w->k_in;
+    if (nnz_blocks) *nnz_blocks = w->nnzb;
+    return SL_OK;
+}
+
+sl_status sparse_linear_export_bsr(const sl_packed_weight *w, uint32_t *row_ptr, uint16_t *col, int8_t *vals)
+{
+    clear_error();
+    if (!w) {
+        set_error("w must not be NULL");
+        return SL_ERR_INVALID_ARG;
+    }
+    if (row_ptr) memcpy(row_ptr, w->row_ptr.data(), w->row_ptr.size() * sizeof(uint32_t));
+    if (col && !w->col.empty()) memcpy(col, w->col.data(), w->col.size() * sizeof(uint16_t));
+    if (vals && !w->vals.empty()) memcpy(vals, w->vals.data(), w->vals.size());
+    return SL_OK;
+}
+
+sl_status sparse_linear_tile_stats(const sl_packed_weight *w, int32_t *n_tiles, int64_t *union_cols,
+                                   int64_t *padded_cols, int64_t *image_bytes)
+{
+    clear_error();
+    if (!w) {
+        set_error("w must not be NULL");
+        return SL_ERR_INVALID_ARG;
+    }
+    const TileImage &ti = w->tiles;
+    if (n_tiles) *n_tiles = ti.n_tiles;
+    if (union_cols) *union_cols = ti.union_cols;
+    if (padded_cols) *padded_cols = ti.padded_cols;
+    if (image_bytes)
+        *image_bytes = (int64_t)(ti.seg_ptr.size() * 4 + ti.panel.size() + ti.ucol.size() * 2 +
+                                 (size_t)w->n_out * 8);
+    return SL_OK;
+}
+
+void sparse_linear_free(sl_packed_weight *w)
+{
+    if (!w) return;
+    if (w->on_device) release_image(w);
+    delete w;
+}
+
+const char *sl_status_string(int32_t s)
+{
+    switch (s) {
+    case SL_OK: return "SL_OK";
+    case SL_ERR_INVALID_ARG: return "SL_ERR_INVALID_ARG";
+    case SL_ERR_SHAPE: return "SL_ERR_SHAPE";
+    case SL_ERR_HIP: return "SL_ERR_HIP";
+    case SL_ERR_OOM: return "SL_ERR_OOM";
+    case SL_ERR_UNSUPPORTED: return "SL_ERR_UNSUPPORTED";
+    case SL_ERR_NOT_ON_DEVICE: return "SL_ERR_NOT_ON_DEVICE";
+    default: return "SL_ERR_UNKNOWN";
+    }
+}
+
+const char *sl_last_error(void) { return g_last_error.c_str(); }
+
+int32_t sl_abi_version(void) { return SL_ABI_VERSION; }
+
+}  // extern "C"

@@ -1,0 +1,154 @@
+"""Host-side tests of the C-ABI library (no GPU needed).
+
+* the shared library loads and exports every symbol include/sparse_linear.h declares;
+* the packer's canonical BSR form and its GPU tile image both round-trip to
+  the dense weight, across sparsities, ragged shapes and chunked K;
+* argument validation returns the documented status codes.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2211_07715_amd as sl
+from workloads import make_weight, random_block_sparse
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _header_symbols():
+    with open(os.path.join(ROOT, "include", "sparse_linear.h")) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return set(re.findall(r"\b([a-z_][a-z0-9_]*)\s*\(", text)) - {"if", "sizeof"}
+
+
+def test_library_exports_every_declared_symbol():
+    lib = sl.load()
+    declared = _header_symbols()
+    assert declared == set(sl.EXPORTS), declared ^ set(sl.EXPORTS)
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert lib.sl_abi_version() == 1
+    assert lib.sl_status_string(-2) == b"SL_ERR_SHAPE"
+
+
+def test_library_has_no_cpu_fallback_symbols():
+    # the product library links no oracle code
+    lib = sl.load()
+    for name in ("oracle_linear", "oracle_acc", "oracle_quantize"):
+        with pytest.raises(AttributeError):
+            getattr(lib, name)
+
+
+def _bsr_reference(w):
+    n, k = w.shape
+    blocks = w.reshape(n // 4, 4, k)
+    keep = np.any(blocks != 0, axis=1)  # [n/4, k]
+    row_ptr = np.concatenate([[0], np.cumsum(keep.sum(axis=1))]).astype(np.uint32)
+    g, c = np.nonzero(keep)
+    vals = blocks[g, :, c]
+    return row_ptr, c.astype(np.uint16), vals
+
+
+@pytest.mark.parametrize("n,k,density", [(4, 1, 1.0), (4, 7, 0.5), (16, 64, 0.3), (20, 33, 0.6), (768, 768, 0.2),
+                                         (3072, 768, 0.1), (768, 3072, 0.1), (64, 1500, 0.25), (8, 2049, 0.05),
+                                         (28, 100, 0.0), (12, 64, 1.0)])
+def test_pack_roundtrip(n, k, density):
+    rng = np.random.default_rng(n * 7 + k)
+    w = random_block_sparse(n, k, density, rng)
+    # a stored block may hold zeros; an all-zero surviving block is dropped
+    sw = rng.uniform(0.001, 0.01, n).astype(np.float32)
+    pw = sl.PackedWeight.pack(w, sw, None, host_only=True)
+    assert np.array_equal(pw.unpack(), w)
+    row_ptr, col, vals = pw.export_bsr()
+    r2, c2, v2 = _bsr_reference(w)
+    assert np.array_equal(row_ptr, r2)
+    assert np.array_equal(col, c2)
+    assert np.array_equal(vals, v2)
+    n2, k2, nnzb = pw.info()
+    assert (n2, k2, nnzb) == (n, k, int(r2[-1]))
+    st = pw.tile_stats()
+    assert st["n_tiles"] == (n + 15) // 16
+    assert st["padded_cols"] % 64 == 0 and st["padded_cols"] >= st["union_cols"]
+    # union of a tile >= the largest block-row in it; <= sum of its block-rows
+    assert st["union_cols"] <= nnzb
+    pw.free()
+
+
+def test_pack_union_statistics_match_mask():
+    wd = make_weight(3072, 768, 0.9, seed=0, cfg=1, op=2)
+    pw = sl.PackedWeight.pack(wd["w"], wd["sw"], wd["b"], host_only=True)
+    keep = np.any(wd["w"].reshape(768, 4, 768) != 0, axis=1)
+    tiles = keep.reshape(192, 4, 768).any(axis=1)
+    st = pw.tile_stats()
+    assert st["union_cols"] == int(tiles.sum())
+    assert st["padded_cols"] == int(sum((int(u) + 63) // 64 * 64 for u in tiles.sum(axis=1)))
+
+
+def test_pack_zero_blocks_inside_stored_blocks():
+    w = np.zeros((8, 5), np.int8)
+    w[0, 1] = 3      # block (0, 1) stored, 3 of its values zero
+    w[7, 4] = -127   # block (1, 4)
+    pw = sl.PackedWeight.pack(w, np.ones(8, np.float32), host_only=True)
+    assert pw.nnz_blocks() == 2
+    row_ptr, col, vals = pw.export_bsr()
+    assert list(row_ptr) == [0, 1, 2] and list(col) == [1, 4]
+    assert vals.tolist() == [[3, 0, 0, 0], [0, 0, 0, -127]]
+    assert np.array_equal(pw.unpack(), w)
+
+
+def _raw_pack(w, n, k, bh=4, bw=1, sw=None, bias=None, host=True):
+    lib = sl.load()
+    h = ctypes.c_void_p()
+    fn = lib.sparse_linear_pack_host if host else lib.sparse_linear_pack
+    st = fn(None if w is None else ctypes.c_void_p(w.ctypes.data), n, k, bh, bw,
+            None if sw is None else ctypes.c_void_p(sw.ctypes.data),
+            None if bias is None else ctypes.c_void_p(bias.ctypes.data), ctypes.byref(h))
+    return st, h
+
+
+def test_pack_validation_status_codes():
+    w = np.ones((8, 8), np.int8)
+    sw = np.ones(8, np.float32)
+    assert _raw_pack(w, 8, 8, sw=sw)[0] == 0
+    assert _raw_pack(w, 6, 8, sw=sw)[0] == -2          # n_out % 4
+    assert _raw_pack(w, 0, 8, sw=sw)[0] == -2
+    assert _raw_pack(w, 8, 0, sw=sw)[0] == -2          # k_in < 1
+    assert _raw_pack(w, 8, 70000, sw=sw)[0] == -2      # k_in > 65535
+    assert _raw_pack(w, 8, 8, bh=2, sw=sw)[0] == -1    # block shape
+    assert _raw_pack(w, 8, 8, bw=4, sw=sw)[0] == -1
+    assert _raw_pack(None, 8, 8, sw=sw)[0] == -1       # NULL
+    assert _raw_pack(w, 8, 8, sw=None)[0] == -1
+    bad = sw.copy(); bad[3] = 0.0
+    assert _raw_pack(w, 8, 8, sw=bad)[0] == -1         # non-positive scale
+    bad[3] = np.nan
+    assert _raw_pack(w, 8, 8, sw=bad)[0] == -1
+    b = np.zeros(8, np.float32); b[1] = np.inf
+    assert _raw_pack(w, 8, 8, sw=sw, bias=b)[0] == -1  # non-finite bias
+    st, h = _raw_pack(w, 6, 8, sw=sw)
+    assert st == -2 and not h.value                    # *out cleared on failure
+    assert b"multiple of 4" in sl.load().sl_last_error()
+
+
+def test_run_on_host_handle_is_rejected():
+    lib = sl.load()
+    w = np.ones((8, 8), np.int8)
+    pw = sl.PackedWeight.pack(w, np.ones(8, np.float32), host_only=True)
+    st = lib.sparse_linear_run(pw.handle, ctypes.c_void_p(16), 4, 1.0, 1, 1.0, ctypes.c_void_p(16), None)
+    assert st == -6
+    # argument checks happen before any device work
+    st = lib.sparse_linear_run(None, None, 4, 1.0, 1, 1.0, None, None)
+    assert st == -1
+    lib.sparse_linear_free(None)  # NULL is a no-op
+
+
+def test_quantize_act_argument_checks_without_gpu():
+    lib = sl.load()
+    assert lib.quantize_act(None, 0, 1.0, None, None) == 0      # empty: no-op
+    assert lib.quantize_act(None, -1, 1.0, None, None) == -2
+    assert lib.quantize_act(None, 4, 0.0, None, None) == -1
+    assert lib.quantize_act(None, 4, float("nan"), None, None) == -1
+    assert lib.quantize_act(None, 4, 1.0, None, None) == -1     # NULL buffers
