@@ -147,13 +147,14 @@ sl_status sparse_linear_export_bsr(const sl_packed_weight *w, uint32_t *row_ptr,
 
 /*
  * Statistics of the GPU tile image: n_tiles channel tiles of 16 output
- * channels; union_cols = sum over tiles of the number of distinct stored
- * block columns; padded_cols = the same after padding each tile's k-chunk
- * segments to the matrix-core depth (the contraction length actually issued);
- * image_bytes = bytes of the device image. Any pointer may be NULL.
+ * channels; n_entries = matrix-core instructions issued per 16 tokens over all
+ * tiles (one per 128-column window that holds a stored block of the tile, plus
+ * one per window where some block-row stores 3 or 4 blocks in one aligned
+ * group of 4 columns); n_overflow = the latter; image_bytes = bytes of the
+ * device image. Any pointer may be NULL.
  */
-sl_status sparse_linear_tile_stats(const sl_packed_weight *w, int32_t *n_tiles, int64_t *union_cols,
-                                   int64_t *padded_cols, int64_t *image_bytes);
+sl_status sparse_linear_tile_stats(const sl_packed_weight *w, int32_t *n_tiles, int64_t *n_entries,
+                                   int64_t *n_overflow, int64_t *image_bytes);
 
 /* Free a handle and its device memory (synchronous). NULL is a no-op. */
 void sparse_linear_free(sl_packed_weight *w);

@@ -160,10 +160,10 @@ class PackedWeight:
         return row_ptr, col, vals
 
     def tile_stats(self):
-        nt, uc, pc, ib = ctypes.c_int32(), ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
-        _check(load().sparse_linear_tile_stats(self.handle, ctypes.byref(nt), ctypes.byref(uc), ctypes.byref(pc),
+        nt, ne, no, ib = ctypes.c_int32(), ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+        _check(load().sparse_linear_tile_stats(self.handle, ctypes.byref(nt), ctypes.byref(ne), ctypes.byref(no),
                                                ctypes.byref(ib)), "sparse_linear_tile_stats")
-        return {"n_tiles": nt.value, "union_cols": uc.value, "padded_cols": pc.value, "image_bytes": ib.value}
+        return {"n_tiles": nt.value, "n_entries": ne.value, "n_overflow": no.value, "image_bytes": ib.value}
 
     def run(self, x, x_scale: float, kind: int, out_scale: float = 1.0, out=None, stream=None):
         """Y = epilogue(X W^T) for a CUDA int8 tensor x [M, k_in]; returns Y."""

@@ -22,7 +22,7 @@ BUILD_DIR = os.path.join(ROOT, "_build")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
-HOST_SOURCES = ["api.cpp", "pack.cpp"]
+HOST_SOURCES = ["api.cpp", "pack.cpp", "gelu_table.cpp"]
 HIP_SOURCES = ["kernels.hip"]
 
 
@@ -43,7 +43,7 @@ def build(verbose: bool = False) -> str:
     objs = []
     for src in HOST_SOURCES:
         obj = os.path.join(BUILD_DIR, src + ".o")
-        _run(["g++", "-std=c++17", "-O2", "-fPIC", "-Wall", "-Wextra", "-I", INCLUDE, "-c",
+        _run(["g++", "-std=c++17", "-O2", "-ffp-contract=off", "-fPIC", "-Wall", "-Wextra", "-I", INCLUDE, "-c",
               os.path.join(CSRC, src), "-o", obj], verbose)
         objs.append(obj)
     for src in HIP_SOURCES:

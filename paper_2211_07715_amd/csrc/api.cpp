@@ -173,8 +173,8 @@ sl_status sparse_linear_export_bsr(const sl_packed_weight *w, uint32_t *row_ptr,
     return SL_OK;
 }
 
-sl_status sparse_linear_tile_stats(const sl_packed_weight *w, int32_t *n_tiles, int64_t *union_cols,
-                                   int64_t *padded_cols, int64_t *image_bytes)
+sl_status sparse_linear_tile_stats(const sl_packed_weight *w, int32_t *n_tiles, int64_t *n_entries,
+                                   int64_t *n_overflow, int64_t *image_bytes)
 {
     clear_error();
     if (!w) {
@@ -183,11 +183,10 @@ sl_status sparse_linear_tile_stats(const sl_packed_weight *w, int32_t *n_tiles, 
     }
     const TileImage &ti = w->tiles;
     if (n_tiles) *n_tiles = ti.n_tiles;
-    if (union_cols) *union_cols = ti.union_cols;
-    if (padded_cols) *padded_cols = ti.padded_cols;
+    if (n_entries) *n_entries = ti.n_entries;
+    if (n_overflow) *n_overflow = ti.n_overflow;
     if (image_bytes)
-        *image_bytes = (int64_t)(ti.seg_ptr.size() * 4 + ti.panel.size() + ti.ucol.size() * 2 +
-                                 (size_t)w->n_out * 8);
+        *image_bytes = (int64_t)(ti.main.size() + ti.ovf.size() + ti.ovf_ptr.size() * 4 + (size_t)w->n_out * 8);
     return SL_OK;
 }
 

@@ -1,43 +1,51 @@
 // gfx950 kernels of the sparse INT8 linear layer, and their launchers.
 //
 // Method (Section "Sparse GEMM operators", Figure 1, Algorithm 1): the stored
-// 4x1 weight blocks form the A operand of an int8 dot-product instruction;
-// the input columns named by the weight's mask are gathered ("re-organised")
-// into the B operand; products accumulate in int32; bias and the other
-// post-operators are applied once per output before the store.
+// 4x1 weight blocks are broadcast into one operand of an int8 dot-product
+// instruction, the input columns named by the weight's mask are picked out of
+// the dense input ("re-organised"), products accumulate in int32, and bias and
+// the other post-operators are applied once per output before the store.
 //
-// MI355X mapping used here:
-//  * A workgroup (4 waves) owns a 64-token tile of X and a group of 16-channel
-//    weight tiles. The token tile is staged once per k-chunk into LDS,
-//    transposed to input-column-major order (one LDS row of 64 tokens per
-//    input column), so a gather by column index reads whole LDS rows.
-//  * Each wave owns some channel tiles. Per k-step it loads one 1 KiB A panel
-//    (16 channels x 64 gathered positions, pre-laid-out by the packer in lane
-//    order: one 16-byte load per lane, fully coalesced) and, for each of the 4
-//    16-token subtiles, gathers the matching 16 x 64 int8 B block from LDS and
-//    issues v_mfma_i32_16x16x64_i8 into that subtile's int32 accumulators.
-//  * After the last k-chunk the epilogue (dequantise, bias, GELU(erf),
-//    requantise) runs on the accumulators in registers and each lane stores 4
-//    consecutive channels of one token.
+// MI355X mapping:
+//  * The weight operand is the A operand of v_smfmac_i32_16x16x128_i8, the
+//    4:2-sparse int8 matrix-core instruction: 16 output channels (4
+//    block-rows) x one 128-column window, at most 2 stored values per row in
+//    every aligned group of 4 columns, each with a 2-bit column index. The
+//    packer turns the block mask into these indices, so the matrix core
+//    itself selects the input columns the mask names. Groups where a
+//    block-row stores 3-4 blocks use a second (slot 1) operand on the window.
+//  * A workgroup of WM x WN waves owns TM tokens x NT 16-channel tiles. Per
+//    128-column window it copies its TM x 128 input bytes (row-major, 16-byte
+//    row pad: the B operand is two conflict-free ds_read_b128 per lane) and
+//    its NT weight operands (plus any overflow operands) into LDS with direct
+//    global->LDS loads; each wave reads its operands into registers, starts
+//    the next window's copies into the other buffer, then issues its matrix
+//    instructions, so copies overlap the math.
+//  * After the last window the epilogue (dequantise, bias, GELU(erf),
+//    requantise) runs on the int32 accumulators in registers; each lane holds
+//    the 4 channels of one block-row for one token and stores them together.
 #include <hip/hip_runtime.h>
 #include <math.h>
+#include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <algorithm>
+#include <memory>
 #include <string>
+#include <type_traits>
 
 #include "sl_internal.h"
 
 namespace sl {
 
 typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x8 __attribute__((ext_vector_type(8)));
 
-constexpr int kTM = 64;             // tokens per workgroup tile
-constexpr int kSub = kTM / 16;      // 16-token subtiles per tile
-constexpr int kWaves = 4;           // waves per workgroup
-constexpr int kThreads = kWaves * 64;
-constexpr int kLdsStride = kTM + 8; // bytes per staged input column (8-byte aligned rows)
-constexpr int kXcds = 8;            // accelerator complex dies (each with its own L2)
+constexpr int kXs = kWin + 16;        // LDS bytes per staged token row (pad: conflict-free B reads)
+constexpr int kXRowPieces = kXs / 16; // 16-byte pieces per staged row, the last one padding
+constexpr int kXcds = 8;              // accelerator complex dies, each with its own L2
+constexpr size_t kLdsMax = 160 * 1024; // LDS per workgroup on gfx950
 
 #define HIP_TRY(expr)                                                                     \
     do {                                                                                  \
@@ -54,106 +62,57 @@ struct LinearArgs {
     int64_t m;
     int32_t n;
     int32_t k;
-    const uint32_t *seg_ptr;
-    const int8_t *panel;
-    const uint16_t *ucol;
+    const int8_t *main;
+    const int8_t *ovf;
+    const uint32_t *ovf_ptr;
     const float *w_scale;
     const float *bias;
     float sx;
     float inv_so;
     int32_t n_tiles;
-    int32_t kc;
-    int32_t n_chunks;
-    int32_t tiles_per_group;
-    int32_t n_groups;
-    int32_t vec_stage;  // 1: X rows are 16-byte aligned and k % 16 == 0
+    int32_t n_win;
+    int32_t n_cgroups;  // channel groups of NT tiles
+};
+
+// Workgroup shape: WM x WN waves; a wave owns ST 16-token subtiles x CT
+// 16-channel tiles. One window's LDS buffer is a flat run of 16-byte pieces:
+// the TM staged token rows (9 pieces each, the 9th padding), then NT main
+// operands, then up to NT overflow operands (68 pieces each); each region is
+// padded to a multiple of 64 pieces so that one 64-lane copy instruction never
+// straddles two regions.
+template <int ST, int CT, int WM, int WN>
+struct Shape {
+    static constexpr int NW = WM * WN;
+    static constexpr int NTH = 64 * NW;
+    static constexpr int TM = 16 * ST * WM;  // tokens per workgroup
+    static constexpr int NT = CT * WN;       // channel tiles per workgroup
+    static constexpr int XP = (TM * kXRowPieces + 63) / 64 * 64;
+    static constexpr int AP = (NT * kOpPieces + 63) / 64 * 64;
+    static constexpr int PIECES = XP + 2 * AP;
+    static constexpr int BUF = PIECES * 16;
+    static constexpr int LDS = 2 * BUF;
+    static constexpr int IPW = (PIECES + NTH - 1) / NTH;  // copy instructions per wave per window
+};
+
+// internal kind: GELU + requantisation evaluated with erf (no usable table)
+constexpr int kEpiI8GeluErf = 5;
+
+// The GELU + requantisation step table, passed by value to the kernel of
+// SL_EPI_I8_GELU.
+struct GeluArg {
+    float hinv, off;
+    int32_t nc, pad;
+    GeluCell cell[kGeluCells];
 };
 
 // Workgroups are dispatched round-robin over the XCDs. Renumber them so that
-// each XCD runs a contiguous range of work items (work items that share a
-// token tile are adjacent, so that tile's X rows are fetched into one L2).
+// each XCD runs a contiguous range of work items; adjacent work items share a
+// token tile, so that tile's rows are fetched into one L2.
 __device__ __forceinline__ int64_t xcd_work_index(int64_t bid, int64_t nwg)
 {
     const int64_t q = nwg / kXcds, r = nwg % kXcds;
     const int64_t x = bid % kXcds, j = bid / kXcds;
     return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + j;
-}
-
-// 4x4 byte transpose: out[j] = {r0.byte j, r1.byte j, r2.byte j, r3.byte j}.
-__device__ __forceinline__ void transpose4x4(uint32_t r0, uint32_t r1, uint32_t r2, uint32_t r3, uint32_t out[4])
-{
-    const uint32_t lo01 = __builtin_amdgcn_perm(r1, r0, 0x05010400u);
-    const uint32_t hi01 = __builtin_amdgcn_perm(r1, r0, 0x07030602u);
-    const uint32_t lo23 = __builtin_amdgcn_perm(r3, r2, 0x05010400u);
-    const uint32_t hi23 = __builtin_amdgcn_perm(r3, r2, 0x07030602u);
-    out[0] = __builtin_amdgcn_perm(lo23, lo01, 0x05040100u);
-    out[1] = __builtin_amdgcn_perm(lo23, lo01, 0x07060302u);
-    out[2] = __builtin_amdgcn_perm(hi23, hi01, 0x05040100u);
-    out[3] = __builtin_amdgcn_perm(hi23, hi01, 0x07060302u);
-}
-
-// Stage X[m0 .. m0+63][kbeg .. kbeg+kw) into LDS as xt[kk][t] (row stride
-// kLdsStride), zero for tokens >= m.
-__device__ __forceinline__ void stage_tile(const LinearArgs &a, int64_t m0, int32_t kbeg, int32_t kw,
-                                           uint8_t *lds)
-{
-    const int tid = threadIdx.x;
-    if (a.vec_stage) {
-        const int kg_n = kw / 16;
-        const int units = (kTM / 4) * kg_n;
-        for (int u = tid; u < units; u += kThreads) {
-            const int kg = u % kg_n, tg = u / kg_n;
-            uint4 r[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int64_t tok = m0 + tg * 4 + i;
-                if (tok < a.m)
-                    r[i] = *reinterpret_cast<const uint4 *>(a.x + tok * a.k + kbeg + kg * 16);
-                else
-                    r[i] = make_uint4(0, 0, 0, 0);
-            }
-            uint32_t o[4];
-            uint8_t *dst = lds + (size_t)(kg * 16) * kLdsStride + tg * 4;
-            transpose4x4(r[0].x, r[1].x, r[2].x, r[3].x, o);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) *reinterpret_cast<uint32_t *>(dst + (0 + j) * kLdsStride) = o[j];
-            transpose4x4(r[0].y, r[1].y, r[2].y, r[3].y, o);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) *reinterpret_cast<uint32_t *>(dst + (4 + j) * kLdsStride) = o[j];
-            transpose4x4(r[0].z, r[1].z, r[2].z, r[3].z, o);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) *reinterpret_cast<uint32_t *>(dst + (8 + j) * kLdsStride) = o[j];
-            transpose4x4(r[0].w, r[1].w, r[2].w, r[3].w, o);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) *reinterpret_cast<uint32_t *>(dst + (12 + j) * kLdsStride) = o[j];
-        }
-    } else {
-        const int total = kTM * kw;
-        for (int i = tid; i < total; i += kThreads) {
-            const int t = i / kw, kk = i % kw;
-            const int64_t tok = m0 + t;
-            lds[(size_t)kk * kLdsStride + t] = tok < a.m ? (uint8_t)a.x[tok * a.k + kbeg + kk] : (uint8_t)0;
-        }
-    }
-}
-
-// B operand for one 16-token subtile: lane l (token l%16 of the subtile, lane
-// group l/16) receives the 16 input bytes at the gathered positions
-// 16*(l/16) .. +15 of the k-step, i.e. at the columns cols[0..15].
-__device__ __forceinline__ i32x4 gather_b(const uint8_t *lds, const uint16_t cols[16], int kbeg, int tok)
-{
-    uint32_t w[4];
-#pragma unroll
-    for (int d = 0; d < 4; ++d) {
-        uint32_t v = 0;
-#pragma unroll
-        for (int b = 0; b < 4; ++b) {
-            const uint32_t byte = lds[(size_t)(cols[4 * d + b] - kbeg) * kLdsStride + tok];
-            v |= byte << (8 * b);
-        }
-        w[d] = v;
-    }
-    return i32x4{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
 }
 
 // GELU, erf form, in the same fp32 operation order as the definition.
@@ -177,96 +136,253 @@ __device__ __forceinline__ int32_t requant_i8(float g, float inv_so)
 }
 
 template <int KIND>
-__device__ __forceinline__ void epilogue_store(const LinearArgs &a, const i32x4 acc, int64_t tok, int32_t ch0)
+__device__ __forceinline__ void epilogue_store(const LinearArgs &a, const i32x4 acc, int64_t tok, int32_t ch0,
+                                               const float s[4], const float b[4], const GeluCell *tab,
+                                               float hinv, float off, float cmax)
 {
 #pragma clang fp contract(off)
-    if (tok >= a.m || ch0 >= a.n) return;
-    const int64_t off = tok * a.n + ch0;
+    if (tok >= a.m) return;
+    const int64_t off64 = tok * a.n + ch0;
     if constexpr (KIND == SL_EPI_ACC_I32) {
-        *reinterpret_cast<i32x4 *>(static_cast<int32_t *>(a.y) + off) = acc;
-        return;
+        *reinterpret_cast<i32x4 *>(static_cast<int32_t *>(a.y) + off64) = acc;
+    } else if constexpr (KIND == SL_EPI_I8_GELU) {
+        uint32_t packed = 0;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            float y = (float)acc[r] * s[r];
+            y = y + b[r];
+            const float c = __builtin_amdgcn_fmed3f(__builtin_fmaf(y, hinv, off), 0.0f, cmax);
+            const GeluCell e = tab[(int)c];
+            const int q = y >= e.thr ? e.q_hi : e.q_lo;
+            packed |= ((uint32_t)q & 0xffu) << (8 * r);
+        }
+        *reinterpret_cast<uint32_t *>(static_cast<int8_t *>(a.y) + off64) = packed;
     } else {
-        const float4 sw = *reinterpret_cast<const float4 *>(a.w_scale + ch0);
-        const float4 bb = *reinterpret_cast<const float4 *>(a.bias + ch0);
-        const float swv[4] = {sw.x, sw.y, sw.z, sw.w};
-        const float bv[4] = {bb.x, bb.y, bb.z, bb.w};
         float g[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            const float s = a.sx * swv[r];
-            float y = (float)acc[r] * s;
-            y = y + bv[r];
-            g[r] = (KIND == SL_EPI_F32_GELU || KIND == SL_EPI_I8_GELU) ? gelu_erf(y) : y;
+            float y = (float)acc[r] * s[r];
+            y = y + b[r];
+            g[r] = (KIND == SL_EPI_F32_GELU || KIND == kEpiI8GeluErf) ? gelu_erf(y) : y;
         }
         if constexpr (KIND == SL_EPI_F32 || KIND == SL_EPI_F32_GELU) {
-            *reinterpret_cast<float4 *>(static_cast<float *>(a.y) + off) = make_float4(g[0], g[1], g[2], g[3]);
+            *reinterpret_cast<float4 *>(static_cast<float *>(a.y) + off64) = make_float4(g[0], g[1], g[2], g[3]);
         } else {
             uint32_t packed = 0;
 #pragma unroll
             for (int r = 0; r < 4; ++r) packed |= ((uint32_t)requant_i8(g[r], a.inv_so) & 0xffu) << (8 * r);
-            *reinterpret_cast<uint32_t *>(static_cast<int8_t *>(a.y) + off) = packed;
+            *reinterpret_cast<uint32_t *>(static_cast<int8_t *>(a.y) + off64) = packed;
         }
     }
 }
 
-template <int KIND, int TW>
-__global__ __launch_bounds__(kThreads) void sparse_linear_kernel(LinearArgs a)
+typedef __attribute__((address_space(3))) void lds_void;
+
+// VEC: X rows are 16-byte aligned and k % 16 == 0, so token rows are copied
+// to LDS with 16-byte direct loads; otherwise they are staged byte by byte.
+template <int KIND, int ST, int CT, int WM, int WN, bool VEC>
+__device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const GeluArg *ep)
 {
-    extern __shared__ __align__(16) uint8_t lds[];
+    using S = Shape<ST, CT, WM, WN>;
+    extern __shared__ __attribute__((aligned(16))) int8_t smem[];
+
     const int64_t work = xcd_work_index(blockIdx.x, gridDim.x);
-    const int64_t tt = work / a.n_groups;
-    const int32_t grp = (int32_t)(work % a.n_groups);
-    const int64_t m0 = tt * kTM;
-    const int32_t tile_begin = grp * a.tiles_per_group;
-    const int32_t tile_end = min(a.n_tiles, tile_begin + a.tiles_per_group);
-    const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+    const int64_t mt = work / a.n_cgroups;
+    const int32_t cg = (int32_t)(work % a.n_cgroups);
+    const int64_t m0 = mt * S::TM;
+    const int32_t tile0 = cg * S::NT;
+    const int32_t ntl = min(S::NT, a.n_tiles - tile0);
+    const int tid = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int lane = tid & 63;
+    const int wm = wave % WM, wn = wave / WM;
+    const size_t pstride = (size_t)a.n_tiles + 1;
 
-    i32x4 acc[TW][kSub];
-#pragma unroll
-    for (int i = 0; i < TW; ++i)
-#pragma unroll
-        for (int s = 0; s < kSub; ++s) acc[i][s] = i32x4{0, 0, 0, 0};
+    // per window: bit j set if tile tile0 + j has an overflow operand, and the
+    // index of the workgroup's first overflow operand of the window
+    uint2 *om = reinterpret_cast<uint2 *>(smem + S::LDS);
+    for (int w = tid; w < a.n_win; w += S::NTH) {
+        const uint32_t *p = a.ovf_ptr + (size_t)w * pstride + tile0;
+        uint32_t mask = 0;
+        for (int j = 0; j < ntl; ++j) mask |= (p[j + 1] > p[j] ? 1u : 0u) << j;
+        om[w] = make_uint2(mask, p[0]);
+    }
+    GeluCell *tab = reinterpret_cast<GeluCell *>(smem + S::LDS + ((a.n_win * 8 + 15) & ~15));
+    float hinv = 0.0f, eoff = 0.0f, cmax = 0.0f;
+    if constexpr (KIND == SL_EPI_I8_GELU) {
+        for (int u = tid; u < ep->nc; u += S::NTH) tab[u] = ep->cell[u];
+        hinv = ep->hinv;
+        eoff = ep->off;
+        cmax = (float)(ep->nc - 1);
+    }
 
-    for (int32_t c = 0; c < a.n_chunks; ++c) {
-        const int32_t kbeg = c * a.kc;
-        const int32_t kw = min(a.k, kbeg + a.kc) - kbeg;
-        __syncthreads();
-        stage_tile(a, m0, kbeg, kw, lds);
-        __syncthreads();
+    i32x4 acc[CT][ST];
 #pragma unroll
-        for (int i = 0; i < TW; ++i) {
-            const int32_t t = tile_begin + wave + i * kWaves;
-            if (t >= tile_end) break;
-            const uint32_t s0 = a.seg_ptr[(int64_t)t * a.n_chunks + c];
-            const uint32_t s1 = a.seg_ptr[(int64_t)t * a.n_chunks + c + 1];
-            for (uint32_t s = s0; s < s1; ++s) {
-                const i32x4 av = *reinterpret_cast<const i32x4 *>(a.panel + (int64_t)s * kStepBytes + lane * 16);
-                const uint16_t *uc = a.ucol + (int64_t)s * kStepK + (lane / 16) * 16;
-                uint16_t cols[16];
-                const uint4 c0 = *reinterpret_cast<const uint4 *>(uc);
-                const uint4 c1 = *reinterpret_cast<const uint4 *>(uc + 8);
-                memcpy(cols, &c0, 16);
-                memcpy(cols + 8, &c1, 16);
+    for (int c = 0; c < CT; ++c)
 #pragma unroll
-                for (int sub = 0; sub < kSub; ++sub) {
-                    const i32x4 bv = gather_b(lds, cols, kbeg, sub * 16 + lane % 16);
-                    acc[i][sub] = __builtin_amdgcn_mfma_i32_16x16x64_i8(av, bv, acc[i][sub], 0, 0, 0);
-                }
+        for (int s = 0; s < ST; ++s) acc[c][s] = i32x4{0, 0, 0, 0};
+
+    auto buf = [&](int w) { return smem + (w & 1) * S::BUF; };
+
+    // per copy instruction i of this wave: its region (uniform) and this
+    // lane's window-independent source offset
+    int64_t soff[S::IPW];
+    int32_t slim[S::IPW];
+    bool sval[S::IPW];
+#pragma unroll
+    for (int i = 0; i < S::IPW; ++i) {
+        const int pc = (i * S::NW + wave) * 64 + lane;
+        soff[i] = 0;
+        slim[i] = 0;
+        sval[i] = false;
+        if (pc < S::XP) {
+            if (pc < S::TM * kXRowPieces) {
+                const int r = pc / kXRowPieces, pp = min(pc % kXRowPieces, kXRowPieces - 2);
+                // rows past m and columns past k read valid bytes whose
+                // products are never stored, resp. meet zero weights
+                soff[i] = min(m0 + r, a.m - 1) * a.k + pp * 16;
+                slim[i] = a.k - 16 - pp * 16;
+                sval[i] = true;
             }
+        } else if (pc < S::XP + S::AP) {
+            const int pm = pc - S::XP;
+            soff[i] = (int64_t)tile0 * kOpBytes + pm * 16;
+            sval[i] = pm < ntl * kOpPieces;
+        } else {
+            soff[i] = pc - S::XP - S::AP;  // piece index within the window's overflow run
         }
     }
 
-    // accumulator lane layout of the 16x16 int32 result: lane l holds rows
-    // 4*(l/16) + r (channels), column l%16 (token), r = 0..3
+    // start window w's copies into its buffer (global -> LDS, asynchronous)
+    auto issue = [&](int w) {
+        int8_t *b = buf(w);
+        const uint2 o = om[w];
+        const uint32_t mask = __builtin_amdgcn_readfirstlane(o.x), olo = __builtin_amdgcn_readfirstlane(o.y);
+        const int nov = __builtin_popcount(mask);
 #pragma unroll
-    for (int i = 0; i < TW; ++i) {
-        const int32_t t = tile_begin + wave + i * kWaves;
-        if (t >= tile_end) break;
-        const int32_t ch0 = t * kTileN + 4 * (lane / 16);
+        for (int i = 0; i < S::IPW; ++i) {
+            const int p0 = (i * S::NW + wave) * 64;  // first piece of this copy (uniform)
+            if (p0 >= S::PIECES) break;
+            if (p0 < S::XP) {
+                if constexpr (VEC)
+                    if (sval[i])
+                        __builtin_amdgcn_global_load_lds(a.x + soff[i] + min(w * kWin, slim[i]),
+                                                         (lds_void *)(b + p0 * 16), 16, 0, 0);
+            } else if (p0 < S::XP + S::AP) {
+                if (sval[i])
+                    __builtin_amdgcn_global_load_lds(a.main + (size_t)w * a.n_tiles * kOpBytes + soff[i],
+                                                     (lds_void *)(b + p0 * 16), 16, 0, 0);
+            } else if (soff[i] < (int64_t)nov * kOpPieces) {
+                __builtin_amdgcn_global_load_lds(a.ovf + ((size_t)olo * kOpPieces + soff[i]) * 16,
+                                                 (lds_void *)(b + p0 * 16), 16, 0, 0);
+            }
+        }
+        if constexpr (!VEC) {
+            for (int u = tid; u < S::TM * kWin; u += S::NTH) {
+                const int r = u / kWin, c = u % kWin;
+                const int64_t tok = m0 + r;
+                const int32_t col = w * kWin + c;
+                b[r * kXs + c] = (tok < a.m && col < a.k) ? a.x[tok * a.k + col] : (int8_t)0;
+            }
+        }
+    };
+
+    // this lane's B row offset (token) and 32-column slice of the window
+    const int brow = (wm * ST * 16 + (lane & 15)) * kXs + 32 * (lane >> 4);
+    // this lane's index word: block-row (lane%16)/4, lane group lane/16
+    const int iword = ((lane & 15) >> 2) * 4 + (lane >> 4);
+
+    __syncthreads();  // overflow masks and epilogue table visible
+    issue(0);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+
+    for (int w = 0; w < a.n_win; ++w) {
+        const int8_t *b = buf(w);
+        // operands of window w into registers before window w+1's copies start
+        i32x8 bv[ST];
 #pragma unroll
-        for (int sub = 0; sub < kSub; ++sub)
-            epilogue_store<KIND>(a, acc[i][sub], m0 + sub * 16 + lane % 16, ch0);
+        for (int s = 0; s < ST; ++s) {
+            const int8_t *p = b + brow + s * 16 * kXs;
+            const i32x4 lo = *reinterpret_cast<const i32x4 *>(p);
+            const i32x4 hi = *reinterpret_cast<const i32x4 *>(p + 16);
+            bv[s] = i32x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        }
+        const uint32_t mask = __builtin_amdgcn_readfirstlane(om[w].x);
+        i32x4 av[CT], ao[CT];
+        int ix[CT], io[CT];
+#pragma unroll
+        for (int c = 0; c < CT; ++c) {
+            const int jw = wn * CT + c;
+            if (jw < ntl) {
+                const int8_t *op = b + S::XP * 16 + jw * kOpBytes;
+                av[c] = *reinterpret_cast<const i32x4 *>(op + lane * 16);
+                ix[c] = *reinterpret_cast<const int *>(op + 1024 + iword * 4);
+                if ((mask >> jw) & 1u) {
+                    const int slot = __builtin_popcount(mask & ((1u << jw) - 1u));
+                    const int8_t *oo = b + (S::XP + S::AP) * 16 + slot * kOpBytes;
+                    ao[c] = *reinterpret_cast<const i32x4 *>(oo + lane * 16);
+                    io[c] = *reinterpret_cast<const int *>(oo + 1024 + iword * 4);
+                }
+            }
+        }
+        if (w + 1 < a.n_win) issue(w + 1);
+#pragma unroll
+        for (int c = 0; c < CT; ++c) {
+            const int jw = wn * CT + c;
+            if (jw < ntl) {
+#pragma unroll
+                for (int s = 0; s < ST; ++s)
+                    acc[c][s] = __builtin_amdgcn_smfmac_i32_16x16x128_i8(av[c], bv[s], acc[c][s], ix[c], 0, 0);
+                if ((mask >> jw) & 1u) {
+#pragma unroll
+                    for (int s = 0; s < ST; ++s)
+                        acc[c][s] = __builtin_amdgcn_smfmac_i32_16x16x128_i8(ao[c], bv[s], acc[c][s], io[c], 0, 0);
+                }
+            }
+        }
+        __builtin_amdgcn_s_waitcnt(0);  // this wave's copies of window w+1 have landed
+        __syncthreads();
     }
+
+    // accumulator layout: lane l holds rows 4*(l/16)+r (channels of one
+    // block-row), column l%16 (token), r = 0..3
+#pragma unroll
+    for (int c = 0; c < CT; ++c) {
+        const int32_t t = tile0 + wn * CT + c;
+        if (t >= a.n_tiles) break;
+        const int32_t ch0 = t * kTileN + 4 * (lane >> 4);
+        if (ch0 >= a.n) continue;  // block-rows past n_out in the last tile
+        float s[4] = {0, 0, 0, 0}, bb4[4] = {0, 0, 0, 0};
+        if constexpr (KIND != SL_EPI_ACC_I32) {
+            const float4 sw = *reinterpret_cast<const float4 *>(a.w_scale + ch0);
+            const float4 bb = *reinterpret_cast<const float4 *>(a.bias + ch0);
+            s[0] = a.sx * sw.x;
+            s[1] = a.sx * sw.y;
+            s[2] = a.sx * sw.z;
+            s[3] = a.sx * sw.w;
+            bb4[0] = bb.x;
+            bb4[1] = bb.y;
+            bb4[2] = bb.z;
+            bb4[3] = bb.w;
+        }
+#pragma unroll
+        for (int st = 0; st < ST; ++st)
+            epilogue_store<KIND>(a, acc[c][st], m0 + wm * ST * 16 + st * 16 + (lane & 15), ch0, s, bb4, tab, hinv,
+                                 eoff, cmax);
+    }
+}
+
+template <int KIND, int ST, int CT, int WM, int WN, bool VEC>
+__global__ __launch_bounds__(64 * WM * WN) void sparse_linear_kernel(LinearArgs a)
+{
+    sparse_linear_body<KIND, ST, CT, WM, WN, VEC>(a, nullptr);
+}
+
+template <int ST, int CT, int WM, int WN, bool VEC>
+__global__ __launch_bounds__(64 * WM * WN) void sparse_linear_gelu_kernel(LinearArgs a, GeluArg ep)
+{
+    sparse_linear_body<SL_EPI_I8_GELU, ST, CT, WM, WN, VEC>(a, &ep);
 }
 
 // ---------------------------------------------------------------------------
@@ -323,14 +439,14 @@ static size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 sl_status upload_image(sl_packed_weight *w)
 {
     const TileImage &ti = w->tiles;
-    const size_t b_seg = ti.seg_ptr.size() * sizeof(uint32_t);
-    const size_t b_panel = ti.panel.size();
-    const size_t b_ucol = ti.ucol.size() * sizeof(uint16_t);
+    const size_t b_main = std::max<size_t>(ti.main.size(), 16);
+    const size_t b_ovf = std::max<size_t>(ti.ovf.size(), 16);
+    const size_t b_ptr = ti.ovf_ptr.size() * sizeof(uint32_t);
     const size_t b_vec = (size_t)w->n_out * sizeof(float);
-    const size_t o_seg = 0;
-    const size_t o_panel = align256(o_seg + b_seg);
-    const size_t o_ucol = align256(o_panel + b_panel);
-    const size_t o_sw = align256(o_ucol + b_ucol);
+    const size_t o_main = 0;
+    const size_t o_ovf = align256(o_main + b_main);
+    const size_t o_ptr = align256(o_ovf + b_ovf);
+    const size_t o_sw = align256(o_ptr + b_ptr);
     const size_t o_b = align256(o_sw + b_vec);
     const size_t total = align256(o_b + b_vec);
     void *base = nullptr;
@@ -343,14 +459,14 @@ sl_status upload_image(sl_packed_weight *w)
     w->dev.base = base;
     w->dev.bytes = (int64_t)total;
     w->on_device = true;  // from here on sparse_linear_free releases the memory
-    HIP_TRY(hipMemcpy(p + o_seg, ti.seg_ptr.data(), b_seg, hipMemcpyHostToDevice));
-    if (b_panel) HIP_TRY(hipMemcpy(p + o_panel, ti.panel.data(), b_panel, hipMemcpyHostToDevice));
-    if (b_ucol) HIP_TRY(hipMemcpy(p + o_ucol, ti.ucol.data(), b_ucol, hipMemcpyHostToDevice));
+    if (!ti.main.empty()) HIP_TRY(hipMemcpy(p + o_main, ti.main.data(), ti.main.size(), hipMemcpyHostToDevice));
+    if (!ti.ovf.empty()) HIP_TRY(hipMemcpy(p + o_ovf, ti.ovf.data(), ti.ovf.size(), hipMemcpyHostToDevice));
+    HIP_TRY(hipMemcpy(p + o_ptr, ti.ovf_ptr.data(), b_ptr, hipMemcpyHostToDevice));
     HIP_TRY(hipMemcpy(p + o_sw, w->w_scale.data(), b_vec, hipMemcpyHostToDevice));
     HIP_TRY(hipMemcpy(p + o_b, w->bias.data(), b_vec, hipMemcpyHostToDevice));
-    w->dev.seg_ptr = reinterpret_cast<const uint32_t *>(p + o_seg);
-    w->dev.panel = reinterpret_cast<const int8_t *>(p + o_panel);
-    w->dev.ucol = reinterpret_cast<const uint16_t *>(p + o_ucol);
+    w->dev.main = reinterpret_cast<const int8_t *>(p + o_main);
+    w->dev.ovf = reinterpret_cast<const int8_t *>(p + o_ovf);
+    w->dev.ovf_ptr = reinterpret_cast<const uint32_t *>(p + o_ptr);
     w->dev.w_scale = reinterpret_cast<const float *>(p + o_sw);
     w->dev.bias = reinterpret_cast<const float *>(p + o_b);
     return SL_OK;
@@ -369,29 +485,106 @@ void release_image(sl_packed_weight *w)
     w->on_device = false;
 }
 
-template <int KIND, int TW>
-static sl_status launch_kt(const LinearArgs &a, int64_t nwg, size_t lds_bytes, hipStream_t stream)
+// Workgroup shapes (ST, CT, WM, WN): (16*ST*WM) tokens x (16*CT*WN) channels.
+struct TileCfg {
+    int st, ct, wm, wn;
+    int tm() const { return 16 * st * wm; }
+    int nt() const { return ct * wn; }
+};
+static const TileCfg kCfgs[] = {
+    {4, 3, 2, 4},  // 128 x 192, 8 waves
+    {2, 3, 4, 2},  // 128 x  96, 8 waves
+    {2, 2, 2, 2},  //  64 x  64, 4 waves
+    {1, 2, 2, 2},  //  32 x  64, 4 waves
+    {1, 1, 2, 2},  //  32 x  32, 4 waves
+};
+
+template <int KIND, int ST, int CT, int WM, int WN, bool VEC>
+static sl_status launch_cfg(const LinearArgs &a, const GeluArg *ep, int64_t nwg, hipStream_t stream)
 {
-    static bool attr_done = false;  // benign race: setting the attribute twice is harmless
+    using S = Shape<ST, CT, WM, WN>;
+    const void *fn;
+    if constexpr (KIND == SL_EPI_I8_GELU)
+        fn = reinterpret_cast<const void *>(&sparse_linear_gelu_kernel<ST, CT, WM, WN, VEC>);
+    else
+        fn = reinterpret_cast<const void *>(&sparse_linear_kernel<KIND, ST, CT, WM, WN, VEC>);
+    static bool attr_done = false;  // benign race: setting it twice is harmless
     if (!attr_done) {
-        HIP_TRY(hipFuncSetAttribute(reinterpret_cast<const void *>(&sparse_linear_kernel<KIND, TW>),
-                                    hipFuncAttributeMaxDynamicSharedMemorySize, kChunkMax * kLdsStride));
+        HIP_TRY(hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, kLdsMax));
         attr_done = true;
     }
-    hipLaunchKernelGGL((sparse_linear_kernel<KIND, TW>), dim3((uint32_t)nwg), dim3(kThreads), lds_bytes, stream, a);
+    const size_t lds = (size_t)S::LDS + (((size_t)a.n_win * 8 + 15) & ~(size_t)15) +
+                       (KIND == SL_EPI_I8_GELU ? kGeluCells * sizeof(GeluCell) : 0);
+    if (lds > kLdsMax) {
+        set_error("k_in too large for this workgroup shape's per-window table");
+        return SL_ERR_UNSUPPORTED;
+    }
+    if constexpr (KIND == SL_EPI_I8_GELU)
+        hipLaunchKernelGGL((sparse_linear_gelu_kernel<ST, CT, WM, WN, VEC>), dim3((uint32_t)nwg), dim3(S::NTH), lds,
+                           stream, a, *ep);
+    else
+        hipLaunchKernelGGL((sparse_linear_kernel<KIND, ST, CT, WM, WN, VEC>), dim3((uint32_t)nwg), dim3(S::NTH), lds,
+                           stream, a);
     HIP_TRY(hipGetLastError());
     return SL_OK;
 }
 
-template <int KIND>
-static sl_status launch_kind(const LinearArgs &a, int tw, int64_t nwg, size_t lds_bytes, hipStream_t stream)
+template <int KIND, bool VEC>
+static sl_status launch_kind(const LinearArgs &a, const GeluArg *ep, TileCfg c, int64_t nwg, hipStream_t stream)
 {
-    switch (tw) {
-    case 1: return launch_kt<KIND, 1>(a, nwg, lds_bytes, stream);
-    case 2: return launch_kt<KIND, 2>(a, nwg, lds_bytes, stream);
-    case 3: return launch_kt<KIND, 3>(a, nwg, lds_bytes, stream);
-    default: return launch_kt<KIND, 4>(a, nwg, lds_bytes, stream);
+#define SL_CFG(A_, B_, C_, D_) \
+    if (c.st == A_ && c.ct == B_ && c.wm == C_ && c.wn == D_) \
+        return launch_cfg<KIND, A_, B_, C_, D_, VEC>(a, ep, nwg, stream);
+    SL_CFG(4, 3, 2, 4)
+    SL_CFG(2, 3, 4, 2)
+    SL_CFG(2, 2, 2, 2)
+    SL_CFG(1, 2, 2, 2)
+#undef SL_CFG
+    return launch_cfg<KIND, 1, 1, 2, 2, VEC>(a, ep, nwg, stream);
+}
+
+template <int KIND>
+static sl_status launch_vec(const LinearArgs &a, const GeluArg *ep, TileCfg c, int64_t nwg, hipStream_t stream,
+                            bool vec)
+{
+    return vec ? launch_kind<KIND, true>(a, ep, c, nwg, stream) : launch_kind<KIND, false>(a, ep, c, nwg, stream);
+}
+
+// Pick the workgroup shape: among shapes that give every CU a workgroup,
+// the one with the least L2 traffic (token rows re-read once per channel
+// group, the weight image once per token group); SL_TILE="st,ct,wm,wn"
+// overrides (tuning).
+static TileCfg choose_cfg(int64_t m, const sl_packed_weight *w)
+{
+    static const char *env = getenv("SL_TILE");
+    if (env) {
+        TileCfg c;
+        if (sscanf(env, "%d,%d,%d,%d", &c.st, &c.ct, &c.wm, &c.wn) == 4)
+            for (const TileCfg &k : kCfgs)
+                if (k.st == c.st && k.ct == c.ct && k.wm == c.wm && k.wn == c.wn) return k;
     }
+    const int32_t n_tiles = w->tiles.n_tiles;
+    const double xbytes = (double)m * w->k_in;
+    const double wbytes = (double)w->tiles.main.size() + (double)w->tiles.ovf.size();
+    const TileCfg *best = nullptr, *most = nullptr;
+    double best_cost = 0;
+    int64_t most_wg = 0;
+    for (const TileCfg &c : kCfgs) {
+        const int64_t mt = (m + c.tm() - 1) / c.tm();
+        const int64_t cgs = (n_tiles + c.nt() - 1) / c.nt();
+        const int64_t nwg = mt * cgs;
+        if (nwg > most_wg) {
+            most_wg = nwg;
+            most = &c;
+        }
+        if (nwg < 240) continue;
+        const double cost = xbytes * cgs + wbytes * mt;
+        if (!best || cost < best_cost) {
+            best = &c;
+            best_cost = cost;
+        }
+    }
+    return best ? *best : *most;
 }
 
 sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int64_t m, float sx, int32_t kind,
@@ -411,43 +604,41 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int64_t m, f
     a.m = m;
     a.n = w->n_out;
     a.k = w->k_in;
-    a.seg_ptr = w->dev.seg_ptr;
-    a.panel = w->dev.panel;
-    a.ucol = w->dev.ucol;
+    a.main = w->dev.main;
+    a.ovf = w->dev.ovf;
+    a.ovf_ptr = w->dev.ovf_ptr;
     a.w_scale = w->dev.w_scale;
     a.bias = w->dev.bias;
     a.sx = sx;
     a.inv_so = inv_so;
     a.n_tiles = ti.n_tiles;
-    a.kc = ti.kc;
-    a.n_chunks = ti.n_chunks;
-    a.vec_stage = (w->k_in % 16 == 0) && ((reinterpret_cast<uintptr_t>(x) & 15) == 0);
-
-    const int64_t ntt = (m + kTM - 1) / kTM;
-    // channel tiles per workgroup: as many as keep >= 2 workgroups per CU
-    int tw = 1;
-    for (int cand = 4; cand >= 1; --cand) {
-        const int64_t groups = (ti.n_tiles + kWaves * cand - 1) / (kWaves * cand);
-        if (ntt * groups >= 512) {
-            tw = cand;
-            break;
-        }
-    }
-    a.tiles_per_group = kWaves * tw;
-    a.n_groups = (ti.n_tiles + a.tiles_per_group - 1) / a.tiles_per_group;
-    const int64_t nwg = ntt * a.n_groups;
+    a.n_win = ti.n_win;
+    const bool vec = (w->k_in % 16 == 0) && ((reinterpret_cast<uintptr_t>(x) & 15) == 0);
+    const TileCfg cfg = choose_cfg(m, w);
+    a.n_cgroups = (ti.n_tiles + cfg.nt() - 1) / cfg.nt();
+    const int64_t mt = (m + cfg.tm() - 1) / cfg.tm();
+    const int64_t nwg = mt * a.n_cgroups;
     if (nwg > 0x7fffffff) {
         set_error("m_tokens too large for one launch");
         return SL_ERR_UNSUPPORTED;
     }
-    const size_t lds_bytes = (size_t)ti.kc * kLdsStride;
     hipStream_t s = static_cast<hipStream_t>(stream);
     switch (kind) {
-    case SL_EPI_ACC_I32: return launch_kind<SL_EPI_ACC_I32>(a, tw, nwg, lds_bytes, s);
-    case SL_EPI_F32: return launch_kind<SL_EPI_F32>(a, tw, nwg, lds_bytes, s);
-    case SL_EPI_F32_GELU: return launch_kind<SL_EPI_F32_GELU>(a, tw, nwg, lds_bytes, s);
-    case SL_EPI_I8: return launch_kind<SL_EPI_I8>(a, tw, nwg, lds_bytes, s);
-    default: return launch_kind<SL_EPI_I8_GELU>(a, tw, nwg, lds_bytes, s);
+    case SL_EPI_ACC_I32: return launch_vec<SL_EPI_ACC_I32>(a, nullptr, cfg, nwg, s, vec);
+    case SL_EPI_F32: return launch_vec<SL_EPI_F32>(a, nullptr, cfg, nwg, s, vec);
+    case SL_EPI_F32_GELU: return launch_vec<SL_EPI_F32_GELU>(a, nullptr, cfg, nwg, s, vec);
+    case SL_EPI_I8: return launch_vec<SL_EPI_I8>(a, nullptr, cfg, nwg, s, vec);
+    default: {
+        std::shared_ptr<const GeluTable> tab = gelu_table(inv_so);
+        if (!tab->ok) return launch_vec<kEpiI8GeluErf>(a, nullptr, cfg, nwg, s, vec);
+        GeluArg ga;
+        ga.hinv = tab->hinv;
+        ga.off = tab->off;
+        ga.nc = tab->nc;
+        ga.pad = 0;
+        memcpy(ga.cell, tab->cell, sizeof(ga.cell));
+        return launch_vec<SL_EPI_I8_GELU>(a, &ga, cfg, nwg, s, vec);
+    }
     }
 }
 

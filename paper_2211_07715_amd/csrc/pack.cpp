@@ -5,12 +5,16 @@
 // reorganisation of the input. Appendix "Block-wise structured sparsity": the
 // blocks are 1-D, 4 consecutive output rows at one input column.
 //
-// The GPU image regroups 4 block-rows into a 16-channel tile so that one
-// 16x16x64 int8 matrix-core instruction can take them as its A operand: per
-// (tile, k-chunk) the union of the 4 block-rows' stored columns is listed once,
-// padded to a multiple of 64, and the 16 x |union| weight panel is laid out in
-// the order the instruction's lanes read it (16 bytes per lane per k-step).
-// Positions a block-row does not store hold 0, so the int32 sum is unchanged.
+// The GPU image regroups 4 block-rows into a 16-channel tile, the A operand of
+// the 4:2-sparse matrix-core instruction v_smfmac_i32_16x16x128_i8. In each
+// 128-column window, a block-row's stored blocks fall into aligned groups of 4
+// columns; the instruction takes at most 2 values per row and group, selected
+// by 2-bit column indices -- the block mask becomes the instruction's sparsity
+// index, and the hardware picks the matching input columns, which is the
+// paper's mask-driven reorganisation of the input. The first two stored blocks
+// of every (block-row, group) go to the window's main entry; the rare third
+// and fourth go to an overflow entry on the same window. All 4 rows of a block
+// share its columns, so each stored block is 4 values with one index.
 #include <math.h>
 #include <string.h>
 
@@ -77,74 +81,109 @@ static sl_status build_bsr(const int8_t *w, int32_t n_out, int32_t k_in, sl_pack
     return SL_OK;
 }
 
+// Group g of a window -> (lane group q, value pair t) with entry_group(q, t) == g.
+static void group_slot(int g, int *q, int *t)
+{
+    for (int qq = 0; qq < 4; ++qq)
+        for (int tt = 0; tt < 8; ++tt)
+            if (entry_group(qq, tt) == g) {
+                *q = qq;
+                *t = tt;
+                return;
+            }
+}
+
+// Default index nibble of a pair with no stored value: positions (0, 1).
+constexpr uint32_t kIdleIdx = 0x44444444u;
+
 static sl_status build_tiles(sl_packed_weight *p)
 {
     TileImage &ti = p->tiles;
     const int32_t nbr = p->n_out / 4;
     const int32_t k_in = p->k_in;
     ti.n_tiles = (p->n_out + kTileN - 1) / kTileN;
-    ti.kc = std::min<int32_t>(k_in, kChunkMax);
-    ti.n_chunks = (k_in + ti.kc - 1) / ti.kc;
-    ti.seg_ptr.assign((size_t)ti.n_tiles * ti.n_chunks + 1, 0);
-    ti.panel.clear();
-    ti.ucol.clear();
-    ti.union_cols = 0;
-    ti.padded_cols = 0;
+    ti.n_win = (k_in + kWin - 1) / kWin;
+    const size_t pstride = (size_t)ti.n_tiles + 1;
+    ti.main.assign((size_t)ti.n_win * ti.n_tiles * kOpBytes, 0);
+    ti.ovf.clear();
+    ti.ovf_ptr.assign((size_t)ti.n_win * pstride, 0);
+    ti.n_entries = 0;
+    ti.n_overflow = 0;
 
-    std::vector<uint16_t> uni;
-    std::vector<int32_t> where(k_in, -1);  // position of a column in the current union
-    uint32_t step = 0;
-    for (int32_t t = 0; t < ti.n_tiles; ++t) {
-        const int32_t g0 = 4 * t, g1 = std::min(4 * t + 4, nbr);
-        // cursors into each block-row's ascending column list
-        uint32_t cur[4] = {0, 0, 0, 0};
-        for (int32_t g = g0; g < g1; ++g) cur[g - g0] = p->row_ptr[g];
-        for (int32_t c = 0; c < ti.n_chunks; ++c) {
-            const int32_t kbeg = c * ti.kc, kend = std::min(k_in, kbeg + ti.kc);
-            uni.clear();
-            uint32_t stop[4];
+    int gq[32], gt[32];
+    for (int g = 0; g < 32; ++g) group_slot(g, &gq[g], &gt[g]);
+
+    std::vector<uint32_t> cur(p->row_ptr.begin(), p->row_ptr.end() - 1);  // per block-row cursor
+    int8_t op[2][kOpBytes];
+    uint32_t n_ovf = 0;
+    for (int32_t w = 0; w < ti.n_win; ++w) {
+        const int32_t wbeg = w * kWin, wend = std::min(k_in, wbeg + kWin);
+        for (int32_t t = 0; t < ti.n_tiles; ++t) {
+            ti.ovf_ptr[(size_t)w * pstride + t] = n_ovf;
+            memset(op, 0, sizeof(op));
+            uint32_t idx[2][16];
+            for (int sl = 0; sl < 2; ++sl)
+                for (int i = 0; i < 16; ++i) idx[sl][i] = kIdleIdx;
+            bool used[2] = {false, false};
+            const int32_t g0 = 4 * t, g1 = std::min(4 * t + 4, nbr);
             for (int32_t g = g0; g < g1; ++g) {
-                uint32_t e = cur[g - g0];
-                while (e < p->row_ptr[g + 1] && p->col[e] < kend) {
-                    uni.push_back(p->col[e]);
-                    ++e;
-                }
-                stop[g - g0] = e;
-            }
-            std::sort(uni.begin(), uni.end());
-            uni.erase(std::unique(uni.begin(), uni.end()), uni.end());
-            const int64_t nu = (int64_t)uni.size();
-            const int64_t nsteps = (nu + kStepK - 1) / kStepK;
-            ti.union_cols += nu;
-            ti.padded_cols += nsteps * kStepK;
-            for (int64_t i = 0; i < nu; ++i) where[uni[i]] = (int32_t)i;
-            // column list, padded with the chunk's first column (weight 0 there)
-            const size_t ubase = ti.ucol.size();
-            ti.ucol.resize(ubase + nsteps * kStepK, (uint16_t)kbeg);
-            for (int64_t i = 0; i < nu; ++i) ti.ucol[ubase + i] = uni[i];
-            // panel: position i of the segment lives in k-step i/64, at
-            // lane group (i%64)/16, byte (i%16); row r of the tile = lane%16
-            const size_t pbase = ti.panel.size();
-            ti.panel.resize(pbase + nsteps * kStepBytes, 0);
-            for (int32_t g = g0; g < g1; ++g) {
-                for (uint32_t e = cur[g - g0]; e < stop[g - g0]; ++e) {
-                    const int64_t pos = where[p->col[e]];
-                    const int64_t s = pos / kStepK, q = pos % kStepK;
-                    const int64_t grp = q / 16, byte = q % 16;
-                    for (int r = 0; r < 4; ++r) {
-                        const int64_t row = 4 * (g - g0) + r;  // 0..15 within the tile
-                        const int64_t lane = grp * 16 + row;
-                        ti.panel[pbase + s * kStepBytes + lane * 16 + byte] = p->vals[4 * e + r];
+                const int jb = g - g0;  // block-row within the tile
+                uint32_t e = cur[g];
+                while (e < p->row_ptr[g + 1] && p->col[e] < wend) {
+                    // all stored blocks of this block-row in one aligned 4-column group
+                    const int grp = (p->col[e] - wbeg) / 4;
+                    uint32_t eg[4];
+                    int n = 0;
+                    while (e < p->row_ptr[g + 1] && p->col[e] < wend && (p->col[e] - wbeg) / 4 == grp)
+                        eg[n++] = e++;
+                    const int q = gq[grp], pt = gt[grp];
+                    for (int sl = 0; sl < 2; ++sl) {
+                        const int lo = 2 * sl, hi = std::min(n, lo + 2);
+                        if (hi <= lo) continue;
+                        used[sl] = true;
+                        // positions of the pair's two values, ascending and
+                        // distinct; a lone block is paired with an unused
+                        // position that holds no value
+                        int pos[2];
+                        uint32_t blk[2] = {UINT32_MAX, UINT32_MAX};
+                        pos[0] = (p->col[eg[lo]] - wbeg) % 4;
+                        blk[0] = eg[lo];
+                        if (hi - lo == 2) {
+                            pos[1] = (p->col[eg[lo + 1]] - wbeg) % 4;
+                            blk[1] = eg[lo + 1];
+                        } else if (pos[0] < 3) {
+                            pos[1] = 3;
+                        } else {
+                            pos[0] = 2;
+                            pos[1] = 3;
+                            blk[1] = blk[0];
+                            blk[0] = UINT32_MAX;
+                        }
+                        uint32_t &ix = idx[sl][jb * 4 + q];
+                        ix &= ~(0xFu << (4 * pt));
+                        ix |= (uint32_t)(pos[0] | (pos[1] << 2)) << (4 * pt);
+                        for (int sp = 0; sp < 2; ++sp) {
+                            if (blk[sp] == UINT32_MAX) continue;
+                            for (int r = 0; r < 4; ++r)
+                                op[sl][(16 * q + 4 * jb + r) * 16 + 2 * pt + sp] = p->vals[4 * (size_t)blk[sp] + r];
+                        }
                     }
                 }
-                cur[g - g0] = stop[g - g0];
+                cur[g] = e;
             }
-            for (int64_t i = 0; i < nu; ++i) where[uni[i]] = -1;
-            step += (uint32_t)nsteps;
-            ti.seg_ptr[(size_t)t * ti.n_chunks + c + 1] = step;
+            memcpy(op[0] + 1024, idx[0], 64);
+            memcpy(op[1] + 1024, idx[1], 64);
+            memcpy(&ti.main[((size_t)w * ti.n_tiles + t) * kOpBytes], op[0], kOpBytes);
+            if (used[0]) ti.n_entries++;
+            if (used[1]) {
+                ti.ovf.insert(ti.ovf.end(), op[1], op[1] + kOpBytes);
+                ++n_ovf;
+                ti.n_entries++;
+                ti.n_overflow++;
+            }
         }
+        ti.ovf_ptr[(size_t)w * pstride + ti.n_tiles] = n_ovf;
     }
-    ti.n_steps = step;
     return SL_OK;
 }
 
@@ -168,41 +207,60 @@ sl_status build_host_image(const int8_t *w, int32_t n_out, int32_t k_in, const f
     }
 }
 
-// Inverse of build_tiles: place every panel byte back at (channel, column).
-// Fails if a (channel, column) pair would receive two non-zero values.
+// Inverse of build_tiles: every value of every operand is placed back at the
+// (channel, column) the instruction reads it for. Fails on values beyond the
+// matrix, two values at one position, or a pair whose two positions coincide.
+static sl_status decode_operand(const int8_t *op, int32_t t, int32_t w, const sl_packed_weight *p, int8_t *dense)
+{
+    const int32_t k_in = p->k_in;
+    for (int lane = 0; lane < 64; ++lane) {
+        const int q = lane / 16, i = lane % 16, jb = i / 4;
+        uint32_t ix;
+        memcpy(&ix, op + 1024 + 4 * (jb * 4 + q), 4);
+        for (int pt = 0; pt < 8; ++pt) {
+            const int pos0 = (ix >> (4 * pt)) & 3, pos1 = (ix >> (4 * pt + 2)) & 3;
+            for (int sp = 0; sp < 2; ++sp) {
+                const int8_t v = op[lane * 16 + 2 * pt + sp];
+                if (!v) continue;
+                if (pos0 == pos1) {
+                    set_error("tile image pair has two equal column positions");
+                    return SL_ERR_INVALID_ARG;
+                }
+                const int32_t n = t * kTileN + i;
+                const int32_t col = w * kWin + 4 * entry_group(q, pt) + (sp ? pos1 : pos0);
+                if (n >= p->n_out || col >= k_in) {
+                    set_error("tile image holds a value outside the matrix");
+                    return SL_ERR_INVALID_ARG;
+                }
+                int8_t &d = dense[(size_t)n * k_in + col];
+                if (d) {
+                    set_error("tile image places two values at one weight position");
+                    return SL_ERR_INVALID_ARG;
+                }
+                d = v;
+            }
+        }
+    }
+    return SL_OK;
+}
+
 sl_status decode_tile_image(const sl_packed_weight *p, int8_t *dense)
 {
     const TileImage &ti = p->tiles;
-    const int32_t k_in = p->k_in;
-    memset(dense, 0, (size_t)p->n_out * k_in);
-    for (int32_t t = 0; t < ti.n_tiles; ++t) {
-        for (int32_t c = 0; c < ti.n_chunks; ++c) {
-            const uint32_t s0 = ti.seg_ptr[(size_t)t * ti.n_chunks + c];
-            const uint32_t s1 = ti.seg_ptr[(size_t)t * ti.n_chunks + c + 1];
-            for (uint32_t s = s0; s < s1; ++s) {
-                for (int lane = 0; lane < 64; ++lane) {
-                    const int row = lane % 16, grp = lane / 16;
-                    const int32_t n = t * kTileN + row;
-                    for (int b = 0; b < 16; ++b) {
-                        const int8_t v = ti.panel[(size_t)s * kStepBytes + lane * 16 + b];
-                        if (!v) continue;
-                        if (n >= p->n_out) {
-                            set_error("tile image holds a value beyond n_out");
-                            return SL_ERR_INVALID_ARG;
-                        }
-                        const int32_t u = ti.ucol[(size_t)s * kStepK + grp * 16 + b];
-                        if (u < c * ti.kc || u >= std::min(k_in, (c + 1) * ti.kc)) {
-                            set_error("tile image column outside its chunk");
-                            return SL_ERR_INVALID_ARG;
-                        }
-                        int8_t &d = dense[(size_t)n * k_in + u];
-                        if (d) {
-                            set_error("tile image places two values at one weight position");
-                            return SL_ERR_INVALID_ARG;
-                        }
-                        d = v;
-                    }
-                }
+    const size_t pstride = (size_t)ti.n_tiles + 1;
+    memset(dense, 0, (size_t)p->n_out * p->k_in);
+    for (int32_t w = 0; w < ti.n_win; ++w) {
+        for (int32_t t = 0; t < ti.n_tiles; ++t) {
+            sl_status st = decode_operand(&ti.main[((size_t)w * ti.n_tiles + t) * kOpBytes], t, w, p, dense);
+            if (st != SL_OK) return st;
+            const uint32_t o0 = ti.ovf_ptr[(size_t)w * pstride + t], o1 = ti.ovf_ptr[(size_t)w * pstride + t + 1];
+            if (o1 - o0 > 1) {
+                set_error("tile image has more than one overflow operand for a (window, tile)");
+                return SL_ERR_INVALID_ARG;
+            }
+            for (uint32_t o = o0; o < o1; ++o) {
+                st = decode_operand(&ti.ovf[(size_t)o * kOpBytes], t, w, p, dense);
+                if (st != SL_OK) return st;
             }
         }
     }

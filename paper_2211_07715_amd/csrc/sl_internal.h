@@ -4,6 +4,7 @@
 
 #include <stdint.h>
 
+#include <memory>
 #include <string>
 #include <vector>
 
@@ -11,39 +12,66 @@
 
 namespace sl {
 
-// One channel tile = 16 output channels = 4 block-rows of 4x1 blocks. This is
-// the row count of the 16x16x64 int8 matrix-core instruction's A operand.
+// One channel tile = 16 output channels = 4 block-rows of 4x1 blocks: the
+// row count of the 4:2-sparse int8 matrix-core instruction
+// v_smfmac_i32_16x16x128_i8 (A: 16 rows x 128 columns with at most 2 stored
+// values in every aligned group of 4 columns; B: 128 x 16 dense).
 constexpr int kTileN = 16;
-// Contraction depth of one v_mfma_i32_16x16x64_i8: a tile's gathered column
-// list is padded to a multiple of this.
-constexpr int kStepK = 64;
-// Input columns are processed in chunks of at most this many (one LDS stage).
-constexpr int kChunkMax = 1024;
-// Bytes of one k-step of the A-operand panel: 64 lanes x 16 int8.
-constexpr int kStepBytes = 64 * 16;
+// Input columns per window (the contraction depth of one instruction).
+constexpr int kWin = 128;
+// Column group (of 4 consecutive window columns) that value pair t of a lane
+// in lane group q (q = lane / 16) addresses, as the instruction defines it:
+// the B operand's lane group g holds window columns 32g .. 32g+31 of its token.
+inline int entry_group(int q, int t) { return 8 * (2 * (q & 1) + (t >> 2)) + 4 * (q >> 1) + (t & 3); }
 
+// One instruction operand in the image: 64 lanes x 16 value bytes (lane
+// 16q + i holds row i; byte 2p + s is slot s of value pair p, addressing
+// window column 4 * entry_group(q, p) + its 2-bit index), then the index words
+// of the 16 (block-row jb, lane group q) pairs at word 4 * jb + q (the 4 rows
+// of a block-row share their column positions).
+constexpr int kOpBytes = 64 * 16 + 16 * 4;  // 1088 = 68 pieces of 16 bytes
+constexpr int kOpPieces = kOpBytes / 16;
+
+// GPU image of a packed weight. Per (128-column window w, 16-channel tile t)
+// the main operand holds the first two stored blocks of every (block-row,
+// aligned 4-column group); where a group holds 3 or 4, an overflow operand on
+// the same window holds the rest.
+//   main     [n_win][n_tiles] operands (all-zero where a tile stores nothing)
+//   ovf      overflow operands, window-major then tile
+//   ovf_ptr  [n_win][n_tiles + 1]: overflow operands of (w, t) are
+//            ovf_ptr[w][t] .. ovf_ptr[w][t+1]-1 (0 or 1 of them)
 struct TileImage {
     int32_t n_tiles = 0;
-    int32_t kc = 0;        // chunk width (input columns per LDS stage)
-    int32_t n_chunks = 0;  // ceil(k_in / kc)
-    int64_t n_steps = 0;   // total k-steps over all (tile, chunk) segments
-    int64_t union_cols = 0;
-    int64_t padded_cols = 0;
-    // segment (t, c) covers k-steps seg_ptr[t*n_chunks + c] .. seg_ptr[t*n_chunks + c + 1) - 1
-    std::vector<uint32_t> seg_ptr;
-    // A operand, per k-step: lane l holds 16 bytes; byte b of lane l is channel
-    // 16t + (l % 16) at gathered position 16*(l/16) + b of the k-step.
-    std::vector<int8_t> panel;
-    // input column of each gathered position: [n_steps][64]
-    std::vector<uint16_t> ucol;
+    int32_t n_win = 0;       // ceil(k_in / 128)
+    int64_t n_entries = 0;   // operands holding a stored block = instructions per 16 tokens
+    int64_t n_overflow = 0;  // overflow operands
+    std::vector<int8_t> main;
+    std::vector<int8_t> ovf;
+    std::vector<uint32_t> ovf_ptr;
 };
+
+// Step table of the fused GELU(erf) + int8 requantisation (gelu_table.cpp).
+constexpr int kGeluCells = 448;
+struct GeluCell {
+    float thr;     // first y of the cell whose code is q_hi (+inf: none)
+    int8_t q_lo;   // code of the cell's y below thr
+    int8_t q_hi;   // code from thr on
+    int16_t pad;
+};
+struct GeluTable {
+    float hinv = 0, off = 0;  // cell(y) = clamp(trunc(fma(y, hinv, off)), 0, nc - 1)
+    int32_t nc = 0;
+    bool ok = false;          // false: a cell would hold two changes; use erf
+    GeluCell cell[kGeluCells];
+};
+std::shared_ptr<const GeluTable> gelu_table(float inv_so);
 
 struct DeviceImage {
     int device = -1;
     void *base = nullptr;  // one allocation holding everything below
-    const uint32_t *seg_ptr = nullptr;
-    const int8_t *panel = nullptr;
-    const uint16_t *ucol = nullptr;
+    const int8_t *main = nullptr;
+    const int8_t *ovf = nullptr;
+    const uint32_t *ovf_ptr = nullptr;
     const float *w_scale = nullptr;
     const float *bias = nullptr;
     int64_t bytes = 0;

@@ -72,20 +72,50 @@ def test_pack_roundtrip(n, k, density):
     assert (n2, k2, nnzb) == (n, k, int(r2[-1]))
     st = pw.tile_stats()
     assert st["n_tiles"] == (n + 15) // 16
-    assert st["padded_cols"] % 64 == 0 and st["padded_cols"] >= st["union_cols"]
-    # union of a tile >= the largest block-row in it; <= sum of its block-rows
-    assert st["union_cols"] <= nnzb
+    assert 0 <= st["n_overflow"] <= st["n_entries"]
+    _check_entry_counts(w, st)
     pw.free()
 
 
-def test_pack_union_statistics_match_mask():
+def _check_entry_counts(w, st):
+    """Entries = one per (16-channel tile, 128-column window) holding a stored
+    block, plus one where a block-row stores 3-4 blocks in an aligned group of
+    4 columns (the 4:2 instruction takes at most 2 per group)."""
+    n, k = w.shape
+    keep = np.any(w.reshape(n // 4, 4, k) != 0, axis=1)          # [brows, k]
+    nbr = n // 4
+    kp = (k + 127) // 128 * 128
+    kk = np.zeros((nbr, kp), bool)
+    kk[:, :k] = keep
+    per_group = kk.reshape(nbr, kp // 4, 4).sum(axis=2)          # [brows, groups]
+    nt = (n + 15) // 16
+    pad_rows = nt * 4 - nbr
+    kk = np.concatenate([kk, np.zeros((pad_rows, kp), bool)])
+    per_group = np.concatenate([per_group, np.zeros((pad_rows, kp // 4), per_group.dtype)])
+    win_any = kk.reshape(nt, 4, kp // 128, 128).any(axis=(1, 3))
+    win_ovf = (per_group.reshape(nt, 4, kp // 128, 32) > 2).any(axis=(1, 3))
+    assert st["n_entries"] == int(win_any.sum() + win_ovf.sum())
+    assert st["n_overflow"] == int(win_ovf.sum())
+
+
+def test_pack_entry_statistics_match_mask():
     wd = make_weight(3072, 768, 0.9, seed=0, cfg=1, op=2)
     pw = sl.PackedWeight.pack(wd["w"], wd["sw"], wd["b"], host_only=True)
-    keep = np.any(wd["w"].reshape(768, 4, 768) != 0, axis=1)
-    tiles = keep.reshape(192, 4, 768).any(axis=1)
     st = pw.tile_stats()
-    assert st["union_cols"] == int(tiles.sum())
-    assert st["padded_cols"] == int(sum((int(u) + 63) // 64 * 64 for u in tiles.sum(axis=1)))
+    _check_entry_counts(wd["w"], st)
+    # at 10 % block density about a third of the (tile, window) pairs overflow
+    assert 0.25 < st["n_overflow"] / (st["n_entries"] - st["n_overflow"]) < 0.5
+
+
+def test_pack_dense_groups_need_overflow():
+    # a block-row with all 4 blocks of a group stored needs the overflow entry
+    w = np.zeros((16, 8), np.int8)
+    w[0:4, 0:4] = np.arange(1, 17, dtype=np.int8).reshape(4, 4)
+    w[4:8, 5] = 7
+    pw = sl.PackedWeight.pack(w, np.ones(16, np.float32), host_only=True)
+    st = pw.tile_stats()
+    assert (st["n_entries"], st["n_overflow"]) == (2, 1)
+    assert np.array_equal(pw.unpack(), w)
 
 
 def test_pack_zero_blocks_inside_stored_blocks():
