@@ -75,23 +75,25 @@ struct LinearArgs {
 };
 
 // Workgroup shape: WM x WN waves; a wave owns ST 16-token subtiles x CT
-// 16-channel tiles. One window's LDS buffer is a flat run of 16-byte pieces:
-// the TM staged token rows (9 pieces each, the 9th padding), then NT main
-// operands, then up to NT overflow operands (68 pieces each); each region is
-// padded to a multiple of 64 pieces so that one 64-lane copy instruction never
-// straddles two regions.
-template <int ST, int CT, int WM, int WN>
+// 16-channel tiles; D windows are in flight (D LDS buffers). One window's
+// buffer is a flat run of 16-byte pieces: the TM staged token rows (9 pieces
+// each, the 9th padding), then NT main operands, then up to NT overflow
+// operands (68 pieces each). Each region is padded to a whole number of
+// 64-lane copy instructions per wave, so every wave issues the same fixed
+// number of copies per window and waits can count them.
+template <int ST, int CT, int WM, int WN, int D>
 struct Shape {
     static constexpr int NW = WM * WN;
     static constexpr int NTH = 64 * NW;
     static constexpr int TM = 16 * ST * WM;  // tokens per workgroup
     static constexpr int NT = CT * WN;       // channel tiles per workgroup
-    static constexpr int XP = (TM * kXRowPieces + 63) / 64 * 64;
-    static constexpr int AP = (NT * kOpPieces + 63) / 64 * 64;
-    static constexpr int PIECES = XP + 2 * AP;
-    static constexpr int BUF = PIECES * 16;
-    static constexpr int LDS = 2 * BUF;
-    static constexpr int IPW = (PIECES + NTH - 1) / NTH;  // copy instructions per wave per window
+    static constexpr int CX = (TM * kXRowPieces + NTH - 1) / NTH;  // copies per wave: token rows
+    static constexpr int CA = (NT * kOpPieces + NTH - 1) / NTH;    // copies per wave: operands
+    static constexpr int XP = CX * NTH;
+    static constexpr int AP = CA * NTH;
+    static constexpr int COPIES = CX + 2 * CA;  // per wave per window
+    static constexpr int BUF = (XP + 2 * AP) * 16;
+    static constexpr int LDS = D * BUF;
 };
 
 // internal kind: GELU + requantisation evaluated with erf (no usable table)
@@ -178,12 +180,21 @@ __device__ __forceinline__ void epilogue_store(const LinearArgs &a, const i32x4 
 
 typedef __attribute__((address_space(3))) void lds_void;
 
+// s_waitcnt with only the vector-memory count constrained (<= N outstanding)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_le()
+{
+    static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+    // gfx9 encoding: vmcnt [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8]
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
 // VEC: X rows are 16-byte aligned and k % 16 == 0, so token rows are copied
 // to LDS with 16-byte direct loads; otherwise they are staged byte by byte.
-template <int KIND, int ST, int CT, int WM, int WN, bool VEC>
+template <int KIND, int ST, int CT, int WM, int WN, int D, bool VEC>
 __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const GeluArg *ep)
 {
-    using S = Shape<ST, CT, WM, WN>;
+    using S = Shape<ST, CT, WM, WN, D>;
     extern __shared__ __attribute__((aligned(16))) int8_t smem[];
 
     const int64_t work = xcd_work_index(blockIdx.x, gridDim.x);
@@ -222,60 +233,54 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
 #pragma unroll
         for (int s = 0; s < ST; ++s) acc[c][s] = i32x4{0, 0, 0, 0};
 
-    auto buf = [&](int w) { return smem + (w & 1) * S::BUF; };
-
-    // per copy instruction i of this wave: its region (uniform) and this
-    // lane's window-independent source offset
-    int64_t soff[S::IPW];
-    int32_t slim[S::IPW];
-    bool sval[S::IPW];
+    // Copy sources, window-independent parts, per copy of this lane. A lane
+    // without data copies valid bytes into padding: copies whose products are
+    // never stored (rows past m) or meet zero weights (columns past k), or
+    // operand slots no wave reads.
+    const int8_t *xsrc[S::CX];
+    int32_t xlim[S::CX];
 #pragma unroll
-    for (int i = 0; i < S::IPW; ++i) {
+    for (int i = 0; i < S::CX; ++i) {
         const int pc = (i * S::NW + wave) * 64 + lane;
-        soff[i] = 0;
-        slim[i] = 0;
-        sval[i] = false;
-        if (pc < S::XP) {
-            if (pc < S::TM * kXRowPieces) {
-                const int r = pc / kXRowPieces, pp = min(pc % kXRowPieces, kXRowPieces - 2);
-                // rows past m and columns past k read valid bytes whose
-                // products are never stored, resp. meet zero weights
-                soff[i] = min(m0 + r, a.m - 1) * a.k + pp * 16;
-                slim[i] = a.k - 16 - pp * 16;
-                sval[i] = true;
-            }
-        } else if (pc < S::XP + S::AP) {
-            const int pm = pc - S::XP;
-            soff[i] = (int64_t)tile0 * kOpBytes + pm * 16;
-            sval[i] = pm < ntl * kOpPieces;
-        } else {
-            soff[i] = pc - S::XP - S::AP;  // piece index within the window's overflow run
-        }
+        const int r = min(pc / kXRowPieces, S::TM - 1), pp = min(pc % kXRowPieces, kXRowPieces - 2);
+        xsrc[i] = a.x + min(m0 + r, a.m - 1) * a.k + pp * 16;
+        xlim[i] = a.k - 16 - pp * 16;
     }
-
-    // start window w's copies into its buffer (global -> LDS, asynchronous)
-    auto issue = [&](int w) {
-        int8_t *b = buf(w);
-        const uint2 o = om[w];
-        const uint32_t mask = __builtin_amdgcn_readfirstlane(o.x), olo = __builtin_amdgcn_readfirstlane(o.y);
-        const int nov = __builtin_popcount(mask);
+    int32_t apiece[S::CA];
 #pragma unroll
-        for (int i = 0; i < S::IPW; ++i) {
-            const int p0 = (i * S::NW + wave) * 64;  // first piece of this copy (uniform)
-            if (p0 >= S::PIECES) break;
-            if (p0 < S::XP) {
-                if constexpr (VEC)
-                    if (sval[i])
-                        __builtin_amdgcn_global_load_lds(a.x + soff[i] + min(w * kWin, slim[i]),
-                                                         (lds_void *)(b + p0 * 16), 16, 0, 0);
-            } else if (p0 < S::XP + S::AP) {
-                if (sval[i])
-                    __builtin_amdgcn_global_load_lds(a.main + (size_t)w * a.n_tiles * kOpBytes + soff[i],
-                                                     (lds_void *)(b + p0 * 16), 16, 0, 0);
-            } else if (soff[i] < (int64_t)nov * kOpPieces) {
-                __builtin_amdgcn_global_load_lds(a.ovf + ((size_t)olo * kOpPieces + soff[i]) * 16,
-                                                 (lds_void *)(b + p0 * 16), 16, 0, 0);
+    for (int i = 0; i < S::CA; ++i) apiece[i] = (i * S::NW + wave) * 64 + lane;
+    const int8_t *main0 = a.main + (size_t)tile0 * kOpBytes;
+
+    // start window w's copies into buffer slot (global -> LDS, asynchronous)
+    // o: the window's overflow mask entry, read by the caller
+    auto issue = [&](int w, int slot, uint2 o) {
+        int8_t *b = smem + slot * S::BUF;
+        if (w >= a.n_win) w = a.n_win - 1;  // past the end: harmless repeat keeps the copy count fixed
+        const uint32_t olo = __builtin_amdgcn_readfirstlane(o.y);
+        const int nov = __builtin_popcount(__builtin_amdgcn_readfirstlane(o.x));
+        // (without VEC the X rows are staged below and every step waits for
+        // all copies, so the copy count need not be fixed)
+        if constexpr (VEC) {
+#pragma unroll
+            for (int i = 0; i < S::CX; ++i) {
+                const int p0 = (i * S::NW + wave) * 64;
+                __builtin_amdgcn_global_load_lds(xsrc[i] + min(w * kWin, xlim[i]), (lds_void *)(b + p0 * 16), 16, 0,
+                                                 0);
             }
+        }
+        const int8_t *mw = main0 + (size_t)w * a.n_tiles * kOpBytes;
+#pragma unroll
+        for (int i = 0; i < S::CA; ++i) {
+            const int p0 = S::XP + (i * S::NW + wave) * 64;
+            const int8_t *src = apiece[i] < ntl * kOpPieces ? mw + apiece[i] * 16 : a.main;
+            __builtin_amdgcn_global_load_lds(src, (lds_void *)(b + p0 * 16), 16, 0, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < S::CA; ++i) {
+            const int p0 = S::XP + S::AP + (i * S::NW + wave) * 64;
+            const int8_t *src =
+                apiece[i] < nov * kOpPieces ? a.ovf + ((size_t)olo * kOpPieces + apiece[i]) * 16 : a.ovf;
+            __builtin_amdgcn_global_load_lds(src, (lds_void *)(b + p0 * 16), 16, 0, 0);
         }
         if constexpr (!VEC) {
             for (int u = tid; u < S::TM * kWin; u += S::NTH) {
@@ -292,14 +297,20 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
     // this lane's index word: block-row (lane%16)/4, lane group lane/16
     const int iword = ((lane & 15) >> 2) * 4 + (lane >> 4);
 
-    __syncthreads();  // overflow masks and epilogue table visible
-    issue(0);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-
-    for (int w = 0; w < a.n_win; ++w) {
-        const int8_t *b = buf(w);
-        // operands of window w into registers before window w+1's copies start
+    auto step = [&](int w, int slot) {
+        // window w (slot) has landed for this wave once at most D-2 later
+        // windows' copies are outstanding; the barrier makes all waves' visible
+        if constexpr (VEC)
+            wait_vmcnt_le<(D - 2) * S::COPIES>();
+        else
+            __builtin_amdgcn_s_waitcnt(0);
+        // a bare barrier: __syncthreads() would also wait for the later
+        // windows' copies still in flight. The loop writes LDS only through
+        // those counted copies; the clobber keeps the compiler from moving
+        // LDS reads across the barrier.
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        const int8_t *b = smem + slot * S::BUF;
         i32x8 bv[ST];
 #pragma unroll
         for (int s = 0; s < ST; ++s) {
@@ -309,24 +320,26 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
             bv[s] = i32x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
         }
         const uint32_t mask = __builtin_amdgcn_readfirstlane(om[w].x);
+        // read here, with this window's reads, rather than after the first
+        // copies of the step: the compiler drains all copies before an LDS
+        // read it cannot separate from them
+        const int wn1 = min(w + D - 1, a.n_win - 1);
+        const uint2 onext = make_uint2(om[wn1].x, om[wn1].y);
         i32x4 av[CT], ao[CT];
         int ix[CT], io[CT];
 #pragma unroll
         for (int c = 0; c < CT; ++c) {
             const int jw = wn * CT + c;
-            if (jw < ntl) {
-                const int8_t *op = b + S::XP * 16 + jw * kOpBytes;
-                av[c] = *reinterpret_cast<const i32x4 *>(op + lane * 16);
-                ix[c] = *reinterpret_cast<const int *>(op + 1024 + iword * 4);
-                if ((mask >> jw) & 1u) {
-                    const int slot = __builtin_popcount(mask & ((1u << jw) - 1u));
-                    const int8_t *oo = b + (S::XP + S::AP) * 16 + slot * kOpBytes;
-                    ao[c] = *reinterpret_cast<const i32x4 *>(oo + lane * 16);
-                    io[c] = *reinterpret_cast<const int *>(oo + 1024 + iword * 4);
-                }
-            }
+            const int8_t *op = b + S::XP * 16 + jw * kOpBytes;
+            av[c] = *reinterpret_cast<const i32x4 *>(op + lane * 16);
+            ix[c] = *reinterpret_cast<const int *>(op + 1024 + iword * 4);
+            const int slot1 = __builtin_popcount(mask & ((1u << jw) - 1u));
+            const int8_t *oo = b + (S::XP + S::AP) * 16 + slot1 * kOpBytes;
+            ao[c] = *reinterpret_cast<const i32x4 *>(oo + lane * 16);
+            io[c] = *reinterpret_cast<const int *>(oo + 1024 + iword * 4);
         }
-        if (w + 1 < a.n_win) issue(w + 1);
+        // the buffer read in the previous step is free: refill it
+        issue(w + D - 1, (slot + D - 1) % D, onext);
 #pragma unroll
         for (int c = 0; c < CT; ++c) {
             const int jw = wn * CT + c;
@@ -341,9 +354,23 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
                 }
             }
         }
-        __builtin_amdgcn_s_waitcnt(0);  // this wave's copies of window w+1 have landed
-        __syncthreads();
+    };
+
+    __syncthreads();  // overflow masks and epilogue table visible
+    uint2 o0[D - 1];
+#pragma unroll
+    for (int d = 0; d < D - 1; ++d) o0[d] = make_uint2(om[min(d, a.n_win - 1)].x, om[min(d, a.n_win - 1)].y);
+#pragma unroll
+    for (int d = 0; d < D - 1; ++d) issue(d, d, o0[d]);
+    int w = 0;
+    for (; w + D <= a.n_win; w += D) {
+#pragma unroll
+        for (int u = 0; u < D; ++u) step(w + u, u);
     }
+#pragma unroll
+    for (int u = 0; u < D; ++u)
+        if (w + u < a.n_win) step(w + u, u);
+    __builtin_amdgcn_s_waitcnt(0);  // no copy may land after the workgroup ends
 
     // accumulator layout: lane l holds rows 4*(l/16)+r (channels of one
     // block-row), column l%16 (token), r = 0..3
@@ -373,16 +400,16 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
     }
 }
 
-template <int KIND, int ST, int CT, int WM, int WN, bool VEC>
+template <int KIND, int ST, int CT, int WM, int WN, int D, bool VEC>
 __global__ __launch_bounds__(64 * WM * WN) void sparse_linear_kernel(LinearArgs a)
 {
-    sparse_linear_body<KIND, ST, CT, WM, WN, VEC>(a, nullptr);
+    sparse_linear_body<KIND, ST, CT, WM, WN, D, VEC>(a, nullptr);
 }
 
-template <int ST, int CT, int WM, int WN, bool VEC>
+template <int ST, int CT, int WM, int WN, int D, bool VEC>
 __global__ __launch_bounds__(64 * WM * WN) void sparse_linear_gelu_kernel(LinearArgs a, GeluArg ep)
 {
-    sparse_linear_body<SL_EPI_I8_GELU, ST, CT, WM, WN, VEC>(a, &ep);
+    sparse_linear_body<SL_EPI_I8_GELU, ST, CT, WM, WN, D, VEC>(a, &ep);
 }
 
 // ---------------------------------------------------------------------------
@@ -485,29 +512,29 @@ void release_image(sl_packed_weight *w)
     w->on_device = false;
 }
 
-// Workgroup shapes (ST, CT, WM, WN): (16*ST*WM) tokens x (16*CT*WN) channels.
+// Workgroup shapes (ST, CT, WM, WN, D): (16*ST*WM) tokens x (16*CT*WN)
+// channels, D windows in flight.
 struct TileCfg {
-    int st, ct, wm, wn;
+    int st, ct, wm, wn, d;
     int tm() const { return 16 * st * wm; }
     int nt() const { return ct * wn; }
 };
 static const TileCfg kCfgs[] = {
-    {4, 3, 2, 4},  // 128 x 192, 8 waves
-    {2, 3, 4, 2},  // 128 x  96, 8 waves
-    {2, 2, 2, 2},  //  64 x  64, 4 waves
-    {1, 2, 2, 2},  //  32 x  64, 4 waves
-    {1, 1, 2, 2},  //  32 x  32, 4 waves
+    {2, 3, 4, 2, 3},  // 128 x  96, 8 waves
+    {2, 2, 2, 2, 4},  //  64 x  64, 4 waves
+    {1, 2, 2, 2, 4},  //  32 x  64, 4 waves
+    {1, 1, 2, 2, 4},  //  32 x  32, 4 waves
 };
 
-template <int KIND, int ST, int CT, int WM, int WN, bool VEC>
+template <int KIND, int ST, int CT, int WM, int WN, int D, bool VEC>
 static sl_status launch_cfg(const LinearArgs &a, const GeluArg *ep, int64_t nwg, hipStream_t stream)
 {
-    using S = Shape<ST, CT, WM, WN>;
+    using S = Shape<ST, CT, WM, WN, D>;
     const void *fn;
     if constexpr (KIND == SL_EPI_I8_GELU)
-        fn = reinterpret_cast<const void *>(&sparse_linear_gelu_kernel<ST, CT, WM, WN, VEC>);
+        fn = reinterpret_cast<const void *>(&sparse_linear_gelu_kernel<ST, CT, WM, WN, D, VEC>);
     else
-        fn = reinterpret_cast<const void *>(&sparse_linear_kernel<KIND, ST, CT, WM, WN, VEC>);
+        fn = reinterpret_cast<const void *>(&sparse_linear_kernel<KIND, ST, CT, WM, WN, D, VEC>);
     static bool attr_done = false;  // benign race: setting it twice is harmless
     if (!attr_done) {
         HIP_TRY(hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, kLdsMax));
@@ -520,11 +547,11 @@ static sl_status launch_cfg(const LinearArgs &a, const GeluArg *ep, int64_t nwg,
         return SL_ERR_UNSUPPORTED;
     }
     if constexpr (KIND == SL_EPI_I8_GELU)
-        hipLaunchKernelGGL((sparse_linear_gelu_kernel<ST, CT, WM, WN, VEC>), dim3((uint32_t)nwg), dim3(S::NTH), lds,
-                           stream, a, *ep);
+        hipLaunchKernelGGL((sparse_linear_gelu_kernel<ST, CT, WM, WN, D, VEC>), dim3((uint32_t)nwg), dim3(S::NTH),
+                           lds, stream, a, *ep);
     else
-        hipLaunchKernelGGL((sparse_linear_kernel<KIND, ST, CT, WM, WN, VEC>), dim3((uint32_t)nwg), dim3(S::NTH), lds,
-                           stream, a);
+        hipLaunchKernelGGL((sparse_linear_kernel<KIND, ST, CT, WM, WN, D, VEC>), dim3((uint32_t)nwg), dim3(S::NTH),
+                           lds, stream, a);
     HIP_TRY(hipGetLastError());
     return SL_OK;
 }
@@ -532,15 +559,14 @@ static sl_status launch_cfg(const LinearArgs &a, const GeluArg *ep, int64_t nwg,
 template <int KIND, bool VEC>
 static sl_status launch_kind(const LinearArgs &a, const GeluArg *ep, TileCfg c, int64_t nwg, hipStream_t stream)
 {
-#define SL_CFG(A_, B_, C_, D_) \
-    if (c.st == A_ && c.ct == B_ && c.wm == C_ && c.wn == D_) \
-        return launch_cfg<KIND, A_, B_, C_, D_, VEC>(a, ep, nwg, stream);
-    SL_CFG(4, 3, 2, 4)
-    SL_CFG(2, 3, 4, 2)
-    SL_CFG(2, 2, 2, 2)
-    SL_CFG(1, 2, 2, 2)
+#define SL_CFG(A_, B_, C_, D_, E_)                                                 \
+    if (c.st == A_ && c.ct == B_ && c.wm == C_ && c.wn == D_ && c.d == E_) \
+        return launch_cfg<KIND, A_, B_, C_, D_, E_, VEC>(a, ep, nwg, stream);
+    SL_CFG(2, 3, 4, 2, 3)
+    SL_CFG(2, 2, 2, 2, 4)
+    SL_CFG(1, 2, 2, 2, 4)
 #undef SL_CFG
-    return launch_cfg<KIND, 1, 1, 2, 2, VEC>(a, ep, nwg, stream);
+    return launch_cfg<KIND, 1, 1, 2, 2, 4, VEC>(a, ep, nwg, stream);
 }
 
 template <int KIND>
@@ -553,7 +579,7 @@ static sl_status launch_vec(const LinearArgs &a, const GeluArg *ep, TileCfg c, i
 // Pick the workgroup shape: among shapes that give every CU a workgroup,
 // the one with the least L2 traffic (token rows re-read once per channel
 // group, the weight image once per token group); SL_TILE="st,ct,wm,wn"
-// overrides (tuning).
+// overrides (tuning; unknown shapes are ignored).
 static TileCfg choose_cfg(int64_t m, const sl_packed_weight *w)
 {
     static const char *env = getenv("SL_TILE");
