@@ -13,11 +13,19 @@ input/output buffer sets (> 2x the 256 MB last-level cache) that every step
 reads its activations from HBM, not from a cache warmed by the previous step.
 
 Prints ONE JSON line. ``value`` is effective int8 TOPS over non-zero MACs
-(2 * M * 4 * stored_blocks per linear, summed) per step time. ``roofline``
-describes the slowest kernel of the step against the HBM bound, with its
+(2 * M * 4 * stored_blocks per linear, summed) per step time; the K timed
+steps are bracketed by two HIP events on the launch stream. Afterwards each
+kernel of the step is launched KERNEL_REPS times back to back (same rotating
+buffers) between two events, which gives its average launch duration.
+``roofline`` describes the slowest kernel against the HBM bound: its
 algorithmic bytes (X + Y + canonical packed W + scales) per launch divided by
-its average launch time from HIP events recorded around each launch.
+that duration; ``traffic`` is the counter-measured bytes per launch from
+profiles/traffic.json when that file was taken on the current kernel source.
 ``cpu_baseline`` times the CPU oracle on the same step.
+
+Launch order (used to match profiler dispatches to ops): one step per buffer
+set (set-up), W warm-up steps, K timed steps, then KERNEL_REPS launches of
+each kernel in step order; with --copy-calib, three elementwise copies last.
 """
 from __future__ import annotations
 
@@ -36,6 +44,9 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, published
 MFMA_I8_PEAK_TOPS = 5000.0   # MI355X dense int8 matrix peak, published
 MALL_BYTES = 256 << 20
+COPY_CALIB_BYTES = 256 << 20  # one read and one write of this many bytes per copy launch
+COPY_CALIB_LAUNCHES = 3
+KERNEL_REPS = 50  # launches per kernel in the per-kernel timing leg
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2211_07715_amd", "csrc", "kernels.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
@@ -59,6 +70,9 @@ def parse():
     p.add_argument("--workload", default="c1")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--cpu-seconds", type=float, default=10.0)
+    p.add_argument("--copy-calib", action="store_true",
+                   help="after the timed steps, run a plain elementwise copy of COPY_CALIB_BYTES three times "
+                        "(the reference kernel that scales the HBM byte counters)")
     return p.parse_args()
 
 
@@ -118,14 +132,13 @@ def main():
     del xf_dev
     stream = torch.cuda.current_stream()
 
-    def step(s, ev=None):
-        if ev is not None:
-            ev[0].record(stream)
-        sl.quantize_act(s["xf"], float(sx), out=s["q"], stream=stream)
-        if ev is not None:
-            ev[1].record(stream)
-        prev_key, prev_scale = None, float(sx)
+    def step(s, only=None):
+        # only=j launches just kernel j of the step (0: quantize_act, 1..: the linears)
+        if only is None or only == 0:
+            sl.quantize_act(s["xf"], float(sx), out=s["q"], stream=stream)
         for i, (pw, md) in enumerate(zip(packed, meta)):
+            if only is not None and only != i + 1:
+                continue
             if md["src"] == "seeded":
                 xin, xs = s["q"], float(sx)
             else:
@@ -133,28 +146,39 @@ def main():
                 xin = s[src]
                 xs = next(mm["so"] for mm in meta if mm["key"] == src)
             pw.run(xin, xs, md["kind"], out_scale=md["so"], out=s[md["key"]], stream=stream)
-            if ev is not None:
-                ev[2 + i].record(stream)
 
     n_k = 1 + len(meta)
+    # every buffer set gets valid activations once (set-up, not warm-up)
+    for s in sets:
+        step(s)
     for i in range(args.warmup):
         step(sets[i % n_sets])
     torch.cuda.synchronize()
 
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(n_k + 1)] for _ in range(args.steps)]
+    # ---- timed region: K whole steps, events only around the region
+    e_start, e_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    e_start.record(stream)
     for i in range(args.steps):
-        step(sets[i % n_sets], events[i])
+        step(sets[i % n_sets])
+    e_end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    per_kernel_ms = np.zeros(n_k)
-    for ev in events:
-        for j in range(n_k):
-            per_kernel_ms[j] += ev[j].elapsed_time(ev[j + 1])
-    span_ms = events[0][0].elapsed_time(events[-1][-1])
-    ms_per_step = span_ms / args.steps
-    per_kernel_us = per_kernel_ms / args.steps * 1e3
+    ms_per_step = e_start.elapsed_time(e_end) / args.steps
+
+    # ---- per-kernel launch duration: each kernel of the step alone, KERNEL_REPS
+    # launches back to back over the rotating buffer sets, HIP events on the
+    # launch stream around the group
+    per_kernel_us = np.zeros(n_k)
+    for j in range(n_k):
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ev0.record(stream)
+        for i in range(KERNEL_REPS):
+            step(sets[i % n_sets], only=j)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        per_kernel_us[j] = ev0.elapsed_time(ev1) / KERNEL_REPS * 1e3
 
     # ---- metric
     total_ops = sum(2 * m * 4 * md["nnzb"] for md in meta)
@@ -179,6 +203,15 @@ def main():
     roofline = {"bound": "hbm", "kernel": names[dom], "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                 "algorithmic_bytes": int(kbytes[dom])}
+
+    if args.copy_calib:
+        src = torch.randint(0, 256, (COPY_CALIB_BYTES,), dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(COPY_CALIB_LAUNCHES):
+            torch.bitwise_not(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
 
     # ---- CPU oracle baseline on the same step (bounded by time)
     cpu = None
@@ -220,7 +253,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{wl.name}: {wl.notes}", "m_tokens": m,
                    "ops": [f"{md['key']} {md['n']}x{md['k']} kind={md['kind']} nnzb={md['nnzb']}" for md in meta],
-                   "buffer_sets": n_sets, "wall_s": round(wall, 3)},
+                   "buffer_sets": n_sets, "kernel_reps": KERNEL_REPS, "wall_s": round(wall, 3)},
         "kernels": kernels,
         "roofline": roofline,
         "cpu_baseline": cpu,

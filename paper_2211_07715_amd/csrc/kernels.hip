@@ -14,13 +14,17 @@
 //    packer turns the block mask into these indices, so the matrix core
 //    itself selects the input columns the mask names. Groups where a
 //    block-row stores 3-4 blocks use a second (slot 1) operand on the window.
-//  * A workgroup of WM x WN waves owns TM tokens x NT 16-channel tiles. Per
-//    128-column window it copies its TM x 128 input bytes (row-major, 16-byte
-//    row pad: the B operand is two conflict-free ds_read_b128 per lane) and
-//    its NT weight operands (plus any overflow operands) into LDS with direct
-//    global->LDS loads; each wave reads its operands into registers, starts
-//    the next window's copies into the other buffer, then issues its matrix
-//    instructions, so copies overlap the math.
+//  * A workgroup owns TM tokens x NT 16-channel tiles and has two kinds of
+//    waves. Copy waves stream each 128-column window into LDS with buffer
+//    loads that write LDS directly: the TM input rows (the 16-byte pieces of
+//    each row permuted by an XOR of the row index, so every B operand read is
+//    conflict-free), the NT weight operands and the overflow operands (one
+//    fixed slot per tile). Compute waves (WM x WN, each ST 16-token subtiles
+//    x CT tiles) read a window's operands into registers and issue its
+//    matrix instructions. Windows pass through a ring of D LDS buffers, one
+//    barrier per window; while the matrix cores work on window w, the compute
+//    waves read window w+1 and the copy waves fetch window w+D-1. Overflow
+//    operands are read and multiplied only for tiles that have one.
 //  * After the last window the epilogue (dequantise, bias, GELU(erf),
 //    requantise) runs on the int32 accumulators in registers; each lane holds
 //    the 4 channels of one block-row for one token and stores them together.
@@ -42,9 +46,18 @@ namespace sl {
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x8 __attribute__((ext_vector_type(8)));
 
-constexpr int kXs = kWin + 16;        // LDS bytes per staged token row (pad: conflict-free B reads)
-constexpr int kXRowPieces = kXs / 16; // 16-byte pieces per staged row, the last one padding
 constexpr int kXcds = 8;              // accelerator complex dies, each with its own L2
+// Buffer-load offset past any buffer this library reads (all < 2 GiB): such
+// a lane reads zeros. Buffer word 3 for raw byte loads on gfx9.
+constexpr uint32_t kOob = 0x80000000u;
+constexpr int32_t kRsrcWord3 = 0x00020000;
+constexpr int64_t kMaxBufferBytes = 0x7ff00000;  // per launch: token chunk bytes and weight image
+// L2 prefetch: the compute waves touch every 128-byte line of the window
+// kPrefetchAhead windows ahead with 4-byte buffer loads into a scratch LDS
+// area (kPrefetchLds bytes, never read), so the copies of that window later
+// hit L2 instead of waiting on memory.
+constexpr int kPrefetchAhead = 0;
+constexpr int kPrefetchLds = 256;
 constexpr size_t kLdsMax = 160 * 1024; // LDS per workgroup on gfx950
 
 #define HIP_TRY(expr)                                                                     \
@@ -64,6 +77,8 @@ struct LinearArgs {
     int32_t k;
     const int8_t *main;
     const int8_t *ovf;
+    uint32_t main_bytes;  // image sizes: the range of the buffer loads
+    uint32_t ovf_bytes;
     const uint32_t *ovf_ptr;
     const float *w_scale;
     const float *bias;
@@ -76,25 +91,33 @@ struct LinearArgs {
 
 // Workgroup shape: WM x WN waves; a wave owns ST 16-token subtiles x CT
 // 16-channel tiles; D windows are in flight (D LDS buffers). One window's
-// buffer is a flat run of 16-byte pieces: the TM staged token rows (9 pieces
-// each, the 9th padding), then NT main operands, then up to NT overflow
-// operands (68 pieces each). Each region is padded to a whole number of
+// buffer: the TM staged token rows (128 bytes each, whole 1 KiB copies of 8
+// rows), then NT main operands, then NT overflow operand slots (68 pieces of
+// 16 bytes per operand). Each operand region is padded to a whole number of
 // 64-lane copy instructions per wave, so every wave issues the same fixed
 // number of copies per window and waits can count them.
 template <int ST, int CT, int WM, int WN, int D>
 struct Shape {
-    static constexpr int NW = WM * WN;
-    static constexpr int NTH = 64 * NW;
+    static constexpr int NW = WM * WN;        // compute waves; as many copy waves again
+    static constexpr int NTH = 64 * NW;       // lanes of the compute (and of the copy) waves
+    static constexpr int NTHG = 2 * NTH;      // threads per workgroup
     static constexpr int TM = 16 * ST * WM;  // tokens per workgroup
     static constexpr int NT = CT * WN;       // channel tiles per workgroup
-    static constexpr int CX = (TM * kXRowPieces + NTH - 1) / NTH;  // copies per wave: token rows
-    static constexpr int CA = (NT * kOpPieces + NTH - 1) / NTH;    // copies per wave: operands
-    static constexpr int XP = CX * NTH;
-    static constexpr int AP = CA * NTH;
+    static constexpr int XC = TM / 8;        // 1 KiB token-row copies per window
+    static constexpr int CX = (XC + NW - 1) / NW;                // copies per wave: token rows
+    static constexpr int CA = (NT * kOpPieces + NTH - 1) / NTH;  // copies per wave: each operand region
+    static constexpr int XB = CX * NW * 1024;
+    static constexpr int AB = CA * NTH * 16;
     static constexpr int COPIES = CX + 2 * CA;  // per wave per window
-    static constexpr int BUF = (XP + 2 * AP) * 16;
+    static constexpr int BUF = XB + 2 * AB;
     static constexpr int LDS = D * BUF;
+    static_assert(TM % 8 == 0, "token rows are copied 8 at a time");
 };
+
+// Position of 16-byte piece p of staged token row r: p ^ xsw(r). The 16 rows
+// one B read touches then start in 16 distinct 16-byte bank groups (and any
+// 8 consecutive rows in 8), so the reads are free of bank conflicts.
+__device__ __forceinline__ int xsw(int r) { return (r ^ (r >> 3)) & 7; }
 
 // internal kind: GELU + requantisation evaluated with erf (no usable table)
 constexpr int kEpiI8GeluErf = 5;
@@ -206,22 +229,32 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
     const int tid = threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int lane = tid & 63;
-    const int wm = wave % WM, wn = wave / WM;
+    // waves 0..NW-1 read operands and run the matrix instructions; waves
+    // NW..2NW-1 only issue the copies, so a copy that waits for room in the
+    // memory queue never holds up the math
+    const bool copier = wave >= S::NW;
+    const int pw = copier ? wave - S::NW : 0;  // copy-wave index
+    const int wm = wave % WM, wn = (wave / WM) % WN;
     const size_t pstride = (size_t)a.n_tiles + 1;
 
     // per window: bit j set if tile tile0 + j has an overflow operand, and the
-    // index of the workgroup's first overflow operand of the window
-    uint2 *om = reinterpret_cast<uint2 *>(smem + S::LDS);
-    for (int w = tid; w < a.n_win; w += S::NTH) {
+    // index of the workgroup's first overflow operand of the window (one
+    // round of independent loads per thread)
+    uint2 *om = reinterpret_cast<uint2 *>(smem + S::LDS + kPrefetchLds);
+    for (int w = tid; w < a.n_win; w += S::NTHG) {
         const uint32_t *p = a.ovf_ptr + (size_t)w * pstride + tile0;
+        uint32_t v[S::NT + 1];
+#pragma unroll
+        for (int j = 0; j <= S::NT; ++j) v[j] = j <= ntl ? p[j] : 0u;
         uint32_t mask = 0;
-        for (int j = 0; j < ntl; ++j) mask |= (p[j + 1] > p[j] ? 1u : 0u) << j;
-        om[w] = make_uint2(mask, p[0]);
+#pragma unroll
+        for (int j = 0; j < S::NT; ++j) mask |= (j < ntl && v[j + 1] > v[j] ? 1u : 0u) << j;
+        om[w] = make_uint2(mask, v[0]);
     }
-    GeluCell *tab = reinterpret_cast<GeluCell *>(smem + S::LDS + ((a.n_win * 8 + 15) & ~15));
+    GeluCell *tab = reinterpret_cast<GeluCell *>(smem + S::LDS + kPrefetchLds + ((a.n_win * 8 + 15) & ~15));
     float hinv = 0.0f, eoff = 0.0f, cmax = 0.0f;
     if constexpr (KIND == SL_EPI_I8_GELU) {
-        for (int u = tid; u < ep->nc; u += S::NTH) tab[u] = ep->cell[u];
+        for (int u = tid; u < ep->nc; u += S::NTHG) tab[u] = ep->cell[u];
         hinv = ep->hinv;
         eoff = ep->off;
         cmax = (float)(ep->nc - 1);
@@ -233,144 +266,282 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
 #pragma unroll
         for (int s = 0; s < ST; ++s) acc[c][s] = i32x4{0, 0, 0, 0};
 
-    // Copy sources, window-independent parts, per copy of this lane. A lane
-    // without data copies valid bytes into padding: copies whose products are
-    // never stored (rows past m) or meet zero weights (columns past k), or
-    // operand slots no wave reads.
-    const int8_t *xsrc[S::CX];
-    int32_t xlim[S::CX];
+    // Copies go through buffer loads with a per-lane offset that is fixed
+    // for the launch (the window advance is a scalar offset), so a copy costs
+    // no vector instructions. A lane without data gets an offset past the
+    // buffer and copies zeros: rows past m, operand pieces past the
+    // workgroup's last tile, absent overflow operands.
+    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)a.x, 0, (int)min<int64_t>(a.m * a.k, kMaxBufferBytes), kRsrcWord3);
+    const __amdgpu_buffer_rsrc_t mr = __builtin_amdgcn_make_buffer_rsrc((void *)a.main, 0, (int)a.main_bytes, kRsrcWord3);
+    const __amdgpu_buffer_rsrc_t orc = __builtin_amdgcn_make_buffer_rsrc((void *)a.ovf, 0, (int)a.ovf_bytes, kRsrcWord3);
+    // token-row copy: row start + this lane's (permuted) piece of window 0,
+    // and the last offset inside the row (a ragged last window never reads
+    // past its row, so never past the buffer)
+    uint32_t xoff[S::CX], xlim[S::CX];
 #pragma unroll
     for (int i = 0; i < S::CX; ++i) {
-        const int pc = (i * S::NW + wave) * 64 + lane;
-        const int r = min(pc / kXRowPieces, S::TM - 1), pp = min(pc % kXRowPieces, kXRowPieces - 2);
-        xsrc[i] = a.x + min(m0 + r, a.m - 1) * a.k + pp * 16;
-        xlim[i] = a.k - 16 - pp * 16;
+        const int r = ((i * S::NW + pw) * 64 + lane) / 8;
+        const bool in = r < S::TM && m0 + r < a.m;
+        xoff[i] = in ? (uint32_t)((m0 + r) * a.k + ((lane & 7) ^ xsw(r)) * 16) : kOob;
+        xlim[i] = in ? (uint32_t)((m0 + r) * a.k + a.k - 16) : kOob;
     }
-    int32_t apiece[S::CA];
+    uint32_t aoff[S::CA];  // main operand piece of the workgroup's tile slice
+    int32_t atile[S::CA], apiece16[S::CA];
 #pragma unroll
-    for (int i = 0; i < S::CA; ++i) apiece[i] = (i * S::NW + wave) * 64 + lane;
-    const int8_t *main0 = a.main + (size_t)tile0 * kOpBytes;
+    for (int i = 0; i < S::CA; ++i) {
+        const int piece = (i * S::NW + pw) * 64 + lane;
+        atile[i] = piece / kOpPieces;
+        apiece16[i] = (piece - atile[i] * kOpPieces) * 16;
+        aoff[i] = atile[i] < ntl ? (uint32_t)((tile0 + atile[i]) * kOpBytes + apiece16[i]) : kOob;
+    }
+    const uint32_t wstride = (uint32_t)a.n_tiles * kOpBytes;  // main image bytes per window
 
-    // start window w's copies into buffer slot (global -> LDS, asynchronous)
-    // o: the window's overflow mask entry, read by the caller
-    auto issue = [&](int w, int slot, uint2 o) {
-        int8_t *b = smem + slot * S::BUF;
-        if (w >= a.n_win) w = a.n_win - 1;  // past the end: harmless repeat keeps the copy count fixed
-        const uint32_t olo = __builtin_amdgcn_readfirstlane(o.y);
-        const int nov = __builtin_popcount(__builtin_amdgcn_readfirstlane(o.x));
-        // (without VEC the X rows are staged below and every step waits for
-        // all copies, so the copy count need not be fixed)
-        if constexpr (VEC) {
-#pragma unroll
-            for (int i = 0; i < S::CX; ++i) {
-                const int p0 = (i * S::NW + wave) * 64;
-                __builtin_amdgcn_global_load_lds(xsrc[i] + min(w * kWin, xlim[i]), (lds_void *)(b + p0 * 16), 16, 0,
-                                                 0);
-            }
+    // Copy k (0 <= k < COPIES) of window w into buffer b (global -> LDS,
+    // asynchronous): token rows, then main operands, then overflow operands
+    // into the slot of their tile. mask/olo: the window's overflow entry.
+    auto copy = [&](int k, int w, int8_t *b, uint32_t mask, uint32_t olo) {
+        if (k < S::CX) {
+            if constexpr (VEC)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_void *)(b + (k * S::NW + pw) * 1024), 16,
+                                                         min(xoff[k] + (uint32_t)(w * kWin), xlim[k]), 0, 0, 0);
+        } else if (k < S::CX + S::CA) {
+            const int i = k - S::CX;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(mr, (lds_void *)(b + S::XB + (i * S::NW + pw) * 1024), 16,
+                                                     aoff[i], (uint32_t)w * wstride, 0, 0);
+        } else {
+            const int i = k - S::CX - S::CA;
+            const uint32_t t = (uint32_t)atile[i];
+            const bool has = t < 32u && ((mask >> t) & 1u);
+            const uint32_t rank = __builtin_popcount(mask & ((1u << (t & 31u)) - 1u));
+            const uint32_t o = has ? (olo + rank) * (uint32_t)kOpBytes + (uint32_t)apiece16[i] : kOob;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(orc, (lds_void *)(b + S::XB + S::AB + (i * S::NW + pw) * 1024),
+                                                     16, o, 0, 0, 0);
         }
-        const int8_t *mw = main0 + (size_t)w * a.n_tiles * kOpBytes;
-#pragma unroll
-        for (int i = 0; i < S::CA; ++i) {
-            const int p0 = S::XP + (i * S::NW + wave) * 64;
-            const int8_t *src = apiece[i] < ntl * kOpPieces ? mw + apiece[i] * 16 : a.main;
-            __builtin_amdgcn_global_load_lds(src, (lds_void *)(b + p0 * 16), 16, 0, 0);
-        }
-#pragma unroll
-        for (int i = 0; i < S::CA; ++i) {
-            const int p0 = S::XP + S::AP + (i * S::NW + wave) * 64;
-            const int8_t *src =
-                apiece[i] < nov * kOpPieces ? a.ovf + ((size_t)olo * kOpPieces + apiece[i]) * 16 : a.ovf;
-            __builtin_amdgcn_global_load_lds(src, (lds_void *)(b + p0 * 16), 16, 0, 0);
-        }
+    };
+    // without VEC the copy waves stage the token rows by ordinary stores
+    auto stage_rows = [&](int w, int8_t *b) {
         if constexpr (!VEC) {
-            for (int u = tid; u < S::TM * kWin; u += S::NTH) {
+            for (int u = tid - S::NTH; u < S::TM * kWin; u += S::NTH) {
                 const int r = u / kWin, c = u % kWin;
                 const int64_t tok = m0 + r;
                 const int32_t col = w * kWin + c;
-                b[r * kXs + c] = (tok < a.m && col < a.k) ? a.x[tok * a.k + col] : (int8_t)0;
+                b[r * kWin + (((c >> 4) ^ xsw(r)) << 4) + (c & 15)] =
+                    (tok < a.m && col < a.k) ? a.x[tok * a.k + col] : (int8_t)0;
             }
         }
     };
 
-    // this lane's B row offset (token) and 32-column slice of the window
-    const int brow = (wm * ST * 16 + (lane & 15)) * kXs + 32 * (lane >> 4);
+    // this lane's B rows (token (lane & 15) of each subtile) and 32-column
+    // slice of the window: pieces 2h and 2h+1, h = lane / 16
+    int brow[ST][2];
+#pragma unroll
+    for (int s = 0; s < ST; ++s) {
+        const int r = wm * ST * 16 + s * 16 + (lane & 15);
+        const int p0 = 2 * (lane >> 4);
+        brow[s][0] = r * kWin + ((p0 ^ xsw(r)) << 4);
+        brow[s][1] = r * kWin + (((p0 + 1) ^ xsw(r)) << 4);
+    }
     // this lane's index word: block-row (lane%16)/4, lane group lane/16
     const int iword = ((lane & 15) >> 2) * 4 + (lane >> 4);
 
-    auto step = [&](int w, int slot) {
-        // window w (slot) has landed for this wave once at most D-2 later
-        // windows' copies are outstanding; the barrier makes all waves' visible
+    // Operands of one window in registers: B (token rows), main and overflow
+    // A operands with their index words. Two sets alternate (steps w and w+1).
+    struct Ops {
+        i32x8 bv[ST];
+        i32x4 av[CT], ao[CT];
+        int ix[CT], io[CT];
+    };
+    Ops ops[2];
+    // main operands (B rows, main A and index words) of one window
+    auto read_main = [&](Ops &r, const int8_t *b) {
+#pragma unroll
+        for (int s = 0; s < ST; ++s) {
+            const i32x4 lo = *reinterpret_cast<const i32x4 *>(b + brow[s][0]);
+            const i32x4 hi = *reinterpret_cast<const i32x4 *>(b + brow[s][1]);
+            r.bv[s] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        }
+#pragma unroll
+        for (int c = 0; c < CT; ++c) {
+            const int8_t *op = b + S::XB + (wn * CT + c) * kOpBytes;
+            r.av[c] = *reinterpret_cast<const i32x4 *>(op + lane * 16);
+            r.ix[c] = *reinterpret_cast<const int *>(op + 1024 + iword * 4);
+        }
+    };
+    // overflow operand of tile c of one window (read only if the tile has one)
+    auto read_ovf = [&](Ops &r, const int8_t *b, int c) {
+        const int8_t *oo = b + S::XB + S::AB + (wn * CT + c) * kOpBytes;
+        r.ao[c] = *reinterpret_cast<const i32x4 *>(oo + lane * 16);
+        r.io[c] = *reinterpret_cast<const int *>(oo + 1024 + iword * 4);
+    };
+    auto read_ops = [&](Ops &r, const int8_t *b, uint32_t mask) {
+        read_main(r, b);
+#pragma unroll
+        for (int c = 0; c < CT; ++c)
+            if ((mask >> (wn * CT + c)) & 1u) read_ovf(r, b, c);  // (ao, io used only under the same condition)
+    };
+    // overflow entry of window w (clamped to the last window). Up to 64
+    // windows the entries sit one per lane in registers and a lane read
+    // fetches one without an LDS round trip.
+    uint32_t om_lx = 0, om_ly = 0;
+    auto om_at = [&](int w) {
+        const int wc = min(w, a.n_win - 1);
+        if (a.n_win <= 64)
+            return make_uint2((uint32_t)__builtin_amdgcn_readlane((int)om_lx, wc),
+                              (uint32_t)__builtin_amdgcn_readlane((int)om_ly, wc));
+        return make_uint2(__builtin_amdgcn_readfirstlane(om[wc].x), __builtin_amdgcn_readfirstlane(om[wc].y));
+    };
+
+    // Software pipeline over windows, one barrier per window. In step w
+    //  * the copy waves wait until window w+1 has landed (at most D-3 later
+    //    windows' copies outstanding), pass the barrier, and start the copies
+    //    of window w+D-1 into the buffer of window w-1;
+    //  * the compute waves pass the barrier, read window w+1's operands into
+    //    one register set while the matrix instructions of window w run from
+    //    the other.
+    // The barrier after the copy waves' wait makes window w+1 visible, and
+    // means every compute wave has finished reading window w-1's buffer
+    // (those reads were consumed by the previous step's matrix instructions).
+    static_assert(D >= 3, "the pipeline reads one window ahead of the one it multiplies");
+    constexpr int U = D % 2 ? 2 * D : D;  // unroll: buffer index and register set both repeat
+
+    __syncthreads();  // overflow masks and epilogue table visible
+    if (lane < a.n_win) {
+        om_lx = om[lane].x;
+        om_ly = om[lane].y;
+    }
+    if (copier) {
+        auto cstep = [&](int w, int u) {
+            if (w + 1 < a.n_win) {
+                if constexpr (VEC)
+                    wait_vmcnt_le<(D - 3) * S::COPIES>();
+                else
+                    __builtin_amdgcn_s_waitcnt(0);
+            }
+            // a bare barrier: __syncthreads() would also wait for the later
+            // windows' copies still in flight
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");
+            // past the end: a harmless repeat keeps the copy count fixed
+            const int wcp = min(w + D - 1, a.n_win - 1);
+            const uint2 o = om_at(wcp);
+            int8_t *nb = smem + ((u + D - 1) % D) * S::BUF;
+#pragma unroll
+            for (int k = 0; k < S::COPIES; ++k) copy(k, wcp, nb, o.x, o.y);
+            stage_rows(wcp, nb);
+        };
+#pragma unroll
+        for (int d = 0; d < D - 1; ++d) {
+            const int wd = min(d, a.n_win - 1);
+            const uint2 od = om_at(wd);
+#pragma unroll
+            for (int k = 0; k < S::COPIES; ++k) copy(k, wd, smem + d * S::BUF, od.x, od.y);
+            stage_rows(wd, smem + d * S::BUF);
+        }
         if constexpr (VEC)
             wait_vmcnt_le<(D - 2) * S::COPIES>();
         else
             __builtin_amdgcn_s_waitcnt(0);
-        // a bare barrier: __syncthreads() would also wait for the later
-        // windows' copies still in flight. The loop writes LDS only through
-        // those counted copies; the clobber keeps the compiler from moving
-        // LDS reads across the barrier.
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
-        const int8_t *b = smem + slot * S::BUF;
-        i32x8 bv[ST];
+        int w = 0;
+        for (; w + U <= a.n_win; w += U) {
 #pragma unroll
-        for (int s = 0; s < ST; ++s) {
-            const int8_t *p = b + brow + s * 16 * kXs;
-            const i32x4 lo = *reinterpret_cast<const i32x4 *>(p);
-            const i32x4 hi = *reinterpret_cast<const i32x4 *>(p + 16);
-            bv[s] = i32x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+            for (int u = 0; u < U; ++u) cstep(w + u, u);
         }
-        const uint32_t mask = __builtin_amdgcn_readfirstlane(om[w].x);
-        // read here, with this window's reads, rather than after the first
-        // copies of the step: the compiler drains all copies before an LDS
-        // read it cannot separate from them
-        const int wn1 = min(w + D - 1, a.n_win - 1);
-        const uint2 onext = make_uint2(om[wn1].x, om[wn1].y);
-        i32x4 av[CT], ao[CT];
-        int ix[CT], io[CT];
 #pragma unroll
-        for (int c = 0; c < CT; ++c) {
-            const int jw = wn * CT + c;
-            const int8_t *op = b + S::XP * 16 + jw * kOpBytes;
-            av[c] = *reinterpret_cast<const i32x4 *>(op + lane * 16);
-            ix[c] = *reinterpret_cast<const int *>(op + 1024 + iword * 4);
-            const int slot1 = __builtin_popcount(mask & ((1u << jw) - 1u));
-            const int8_t *oo = b + (S::XP + S::AP) * 16 + slot1 * kOpBytes;
-            ao[c] = *reinterpret_cast<const i32x4 *>(oo + lane * 16);
-            io[c] = *reinterpret_cast<const int *>(oo + 1024 + iword * 4);
-        }
-        // the buffer read in the previous step is free: refill it
-        issue(w + D - 1, (slot + D - 1) % D, onext);
-#pragma unroll
-        for (int c = 0; c < CT; ++c) {
-            const int jw = wn * CT + c;
-            if (jw < ntl) {
-#pragma unroll
-                for (int s = 0; s < ST; ++s)
-                    acc[c][s] = __builtin_amdgcn_smfmac_i32_16x16x128_i8(av[c], bv[s], acc[c][s], ix[c], 0, 0);
-                if ((mask >> jw) & 1u) {
-#pragma unroll
-                    for (int s = 0; s < ST; ++s)
-                        acc[c][s] = __builtin_amdgcn_smfmac_i32_16x16x128_i8(ao[c], bv[s], acc[c][s], io[c], 0, 0);
-                }
-            }
+        for (int u = 0; u < U; ++u)
+            if (w + u < a.n_win) cstep(w + u, u);
+        __builtin_amdgcn_s_waitcnt(0);  // no copy may land after the workgroup ends
+        return;
+    }
+
+    // compute waves. Prefetch duty per wave: waves 0..XI-1 the token rows
+    // (64 per wave), the next wave the main operands, the one after the
+    // overflow operands of the workgroup's tiles.
+    constexpr int XI = (S::TM + 63) / 64;
+    static_assert(XI + 2 <= S::NW, "not enough compute waves for the prefetch duties");
+    const int pf_row = wave * 64 + lane;
+    const uint32_t pf_xoff = (wave < XI && pf_row < S::TM && m0 + pf_row < a.m) ? (uint32_t)((m0 + pf_row) * a.k) : kOob;
+    const uint32_t pf_moff =
+        lane * 128 < ntl * kOpBytes ? (uint32_t)(tile0 * kOpBytes + lane * 128) : kOob;
+    lds_void *pf_dst = (lds_void *)(smem + S::LDS);
+    auto prefetch = [&](int w) {
+        const int wp = min(w, a.n_win - 1);
+        if (wave < XI) {
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, pf_dst, 4, pf_xoff, (uint32_t)(wp * kWin), 0, 0);
+        } else if (wave == XI) {
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(mr, pf_dst, 4, pf_moff, (uint32_t)wp * wstride, 0, 0);
+        } else if (wave == XI + 1) {
+            const uint2 o = om_at(wp);
+            const uint32_t nov = __builtin_popcount(o.x);
+            const uint32_t off = lane * 128u < nov * (uint32_t)kOpBytes ? o.y * (uint32_t)kOpBytes + lane * 128u : kOob;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(orc, pf_dst, 4, off, 0, 0, 0);
         }
     };
 
-    __syncthreads();  // overflow masks and epilogue table visible
-    uint2 o0[D - 1];
+    // mask_w: overflow mask of window w (its operands are in ops[u & 1]);
+    // mask_n: of window w+1
+    uint32_t mask_w, mask_n;
+    auto step = [&](int w, int u) {
+        Ops &cur = ops[u & 1];
+        Ops &nxt = ops[(u + 1) & 1];
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        const uint32_t mask_n2 = om_at(w + 2).x;
+        if constexpr (kPrefetchAhead > 0) prefetch(w + kPrefetchAhead);
+        const int8_t *nb = smem + ((u + 1) % D) * S::BUF;
+        // Main part: window w+1's main operand reads and window w's main
+        // matrix instructions, one after the other, so that a read waiting
+        // for room in the LDS queue does not leave the matrix core idle.
+        // (The last step reads nothing: the barrier has already passed, so
+        // reading a stale buffer is harmless and keeps the code branch-free.)
+        // Main products of tiles past n_tiles land in accumulators that are
+        // never stored, so they need no branch either.
+        read_main(nxt, nb);
 #pragma unroll
-    for (int d = 0; d < D - 1; ++d) o0[d] = make_uint2(om[min(d, a.n_win - 1)].x, om[min(d, a.n_win - 1)].y);
+        for (int c = 0; c < CT; ++c)
 #pragma unroll
-    for (int d = 0; d < D - 1; ++d) issue(d, d, o0[d]);
-    int w = 0;
-    for (; w + D <= a.n_win; w += D) {
+            for (int s = 0; s < ST; ++s)
+                acc[c][s] = __builtin_amdgcn_smfmac_i32_16x16x128_i8(cur.av[c], cur.bv[s], acc[c][s], cur.ix[c], 0, 0);
 #pragma unroll
-        for (int u = 0; u < D; ++u) step(w + u, u);
+        for (int v = 0; v < CT * ST; ++v) {
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one matrix instruction
+        }
+        __builtin_amdgcn_sched_group_barrier(0x100, 2 * ST + 2 * CT, 0);  // the remaining reads
+        // overflow part, per tile
+#pragma unroll
+        for (int c = 0; c < CT; ++c) {
+            const int jw = wn * CT + c;
+            if (w + 1 < a.n_win && ((mask_n >> jw) & 1u)) read_ovf(nxt, nb, c);
+            if ((mask_w >> jw) & 1u) {
+#pragma unroll
+                for (int s = 0; s < ST; ++s)
+                    acc[c][s] =
+                        __builtin_amdgcn_smfmac_i32_16x16x128_i8(cur.ao[c], cur.bv[s], acc[c][s], cur.io[c], 0, 0);
+            }
+        }
+        mask_w = mask_n;
+        mask_n = mask_n2;
+    };
+    if constexpr (kPrefetchAhead > 0)
+        for (int d = D - 1; d < kPrefetchAhead; ++d) prefetch(d);
+    __builtin_amdgcn_s_barrier();  // window 0 has landed
+    asm volatile("" ::: "memory");
+    mask_w = om_at(0).x;
+    mask_n = om_at(1).x;
+    read_ops(ops[0], smem, mask_w);
+    {
+        int w = 0;
+        for (; w + U <= a.n_win; w += U) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) step(w + u, u);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (w + u < a.n_win) step(w + u, u);
     }
-#pragma unroll
-    for (int u = 0; u < D; ++u)
-        if (w + u < a.n_win) step(w + u, u);
-    __builtin_amdgcn_s_waitcnt(0);  // no copy may land after the workgroup ends
 
     // accumulator layout: lane l holds rows 4*(l/16)+r (channels of one
     // block-row), column l%16 (token), r = 0..3
@@ -401,13 +572,13 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
 }
 
 template <int KIND, int ST, int CT, int WM, int WN, int D, bool VEC>
-__global__ __launch_bounds__(64 * WM * WN) void sparse_linear_kernel(LinearArgs a)
+__global__ __launch_bounds__(128 * WM * WN) void sparse_linear_kernel(LinearArgs a)
 {
     sparse_linear_body<KIND, ST, CT, WM, WN, D, VEC>(a, nullptr);
 }
 
 template <int ST, int CT, int WM, int WN, int D, bool VEC>
-__global__ __launch_bounds__(64 * WM * WN) void sparse_linear_gelu_kernel(LinearArgs a, GeluArg ep)
+__global__ __launch_bounds__(128 * WM * WN) void sparse_linear_gelu_kernel(LinearArgs a, GeluArg ep)
 {
     sparse_linear_body<SL_EPI_I8_GELU, ST, CT, WM, WN, D, VEC>(a, &ep);
 }
@@ -466,6 +637,10 @@ static size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 sl_status upload_image(sl_packed_weight *w)
 {
     const TileImage &ti = w->tiles;
+    if ((int64_t)ti.main.size() > kMaxBufferBytes || (int64_t)ti.ovf.size() > kMaxBufferBytes) {
+        set_error("packed weight image over 2 GiB (n_out x k_in too large for one image)");
+        return SL_ERR_UNSUPPORTED;
+    }
     const size_t b_main = std::max<size_t>(ti.main.size(), 16);
     const size_t b_ovf = std::max<size_t>(ti.ovf.size(), 16);
     const size_t b_ptr = ti.ovf_ptr.size() * sizeof(uint32_t);
@@ -520,10 +695,12 @@ struct TileCfg {
     int nt() const { return ct * wn; }
 };
 static const TileCfg kCfgs[] = {
-    {2, 3, 4, 2, 3},  // 128 x  96, 8 waves
-    {2, 2, 2, 2, 4},  //  64 x  64, 4 waves
-    {1, 2, 2, 2, 4},  //  32 x  64, 4 waves
-    {1, 1, 2, 2, 4},  //  32 x  32, 4 waves
+    {4, 3, 2, 2, 3},  // 128 x  96,  96 KiB LDS
+    {4, 3, 2, 2, 4},  // 128 x  96, 128 KiB
+    {2, 3, 2, 2, 3},  //  64 x  96,  72 KiB (two workgroups per CU)
+    {2, 3, 2, 2, 4},  //  64 x  96,  96 KiB
+    {1, 3, 2, 2, 3},  //  32 x  96,  60 KiB
+    {1, 1, 2, 2, 3},  //  32 x  32,  36 KiB
 };
 
 template <int KIND, int ST, int CT, int WM, int WN, int D, bool VEC>
@@ -540,17 +717,17 @@ static sl_status launch_cfg(const LinearArgs &a, const GeluArg *ep, int64_t nwg,
         HIP_TRY(hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, kLdsMax));
         attr_done = true;
     }
-    const size_t lds = (size_t)S::LDS + (((size_t)a.n_win * 8 + 15) & ~(size_t)15) +
+    const size_t lds = (size_t)S::LDS + kPrefetchLds + (((size_t)a.n_win * 8 + 15) & ~(size_t)15) +
                        (KIND == SL_EPI_I8_GELU ? kGeluCells * sizeof(GeluCell) : 0);
     if (lds > kLdsMax) {
         set_error("k_in too large for this workgroup shape's per-window table");
         return SL_ERR_UNSUPPORTED;
     }
     if constexpr (KIND == SL_EPI_I8_GELU)
-        hipLaunchKernelGGL((sparse_linear_gelu_kernel<ST, CT, WM, WN, D, VEC>), dim3((uint32_t)nwg), dim3(S::NTH),
+        hipLaunchKernelGGL((sparse_linear_gelu_kernel<ST, CT, WM, WN, D, VEC>), dim3((uint32_t)nwg), dim3(S::NTHG),
                            lds, stream, a, *ep);
     else
-        hipLaunchKernelGGL((sparse_linear_kernel<KIND, ST, CT, WM, WN, D, VEC>), dim3((uint32_t)nwg), dim3(S::NTH),
+        hipLaunchKernelGGL((sparse_linear_kernel<KIND, ST, CT, WM, WN, D, VEC>), dim3((uint32_t)nwg), dim3(S::NTHG),
                            lds, stream, a);
     HIP_TRY(hipGetLastError());
     return SL_OK;
@@ -559,14 +736,16 @@ static sl_status launch_cfg(const LinearArgs &a, const GeluArg *ep, int64_t nwg,
 template <int KIND, bool VEC>
 static sl_status launch_kind(const LinearArgs &a, const GeluArg *ep, TileCfg c, int64_t nwg, hipStream_t stream)
 {
-#define SL_CFG(A_, B_, C_, D_, E_)                                                 \
+#define SL_CFG(A_, B_, C_, D_, E_)                                         \
     if (c.st == A_ && c.ct == B_ && c.wm == C_ && c.wn == D_ && c.d == E_) \
         return launch_cfg<KIND, A_, B_, C_, D_, E_, VEC>(a, ep, nwg, stream);
-    SL_CFG(2, 3, 4, 2, 3)
-    SL_CFG(2, 2, 2, 2, 4)
-    SL_CFG(1, 2, 2, 2, 4)
+    SL_CFG(4, 3, 2, 2, 3)
+    SL_CFG(4, 3, 2, 2, 4)
+    SL_CFG(2, 3, 2, 2, 3)
+    SL_CFG(2, 3, 2, 2, 4)
+    SL_CFG(1, 3, 2, 2, 3)
 #undef SL_CFG
-    return launch_cfg<KIND, 1, 1, 2, 2, 4, VEC>(a, ep, nwg, stream);
+    return launch_cfg<KIND, 1, 1, 2, 2, 3, VEC>(a, ep, nwg, stream);
 }
 
 template <int KIND>
@@ -578,16 +757,16 @@ static sl_status launch_vec(const LinearArgs &a, const GeluArg *ep, TileCfg c, i
 
 // Pick the workgroup shape: among shapes that give every CU a workgroup,
 // the one with the least L2 traffic (token rows re-read once per channel
-// group, the weight image once per token group); SL_TILE="st,ct,wm,wn"
+// group, the weight image once per token group); SL_TILE="st,ct,wm,wn,d"
 // overrides (tuning; unknown shapes are ignored).
 static TileCfg choose_cfg(int64_t m, const sl_packed_weight *w)
 {
     static const char *env = getenv("SL_TILE");
     if (env) {
         TileCfg c;
-        if (sscanf(env, "%d,%d,%d,%d", &c.st, &c.ct, &c.wm, &c.wn) == 4)
+        if (sscanf(env, "%d,%d,%d,%d,%d", &c.st, &c.ct, &c.wm, &c.wn, &c.d) == 5)
             for (const TileCfg &k : kCfgs)
-                if (k.st == c.st && k.ct == c.ct && k.wm == c.wm && k.wn == c.wn) return k;
+                if (k.st == c.st && k.ct == c.ct && k.wm == c.wm && k.wn == c.wn && k.d == c.d) return k;
     }
     const int32_t n_tiles = w->tiles.n_tiles;
     const double xbytes = (double)m * w->k_in;
@@ -596,6 +775,7 @@ static TileCfg choose_cfg(int64_t m, const sl_packed_weight *w)
     double best_cost = 0;
     int64_t most_wg = 0;
     for (const TileCfg &c : kCfgs) {
+        if (c.d != 4 || c.wm * c.wn != 4) continue;
         const int64_t mt = (m + c.tm() - 1) / c.tm();
         const int64_t cgs = (n_tiles + c.nt() - 1) / c.nt();
         const int64_t nwg = mt * cgs;
@@ -625,13 +805,12 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int64_t m, f
     }
     const TileImage &ti = w->tiles;
     LinearArgs a;
-    a.x = x;
-    a.y = y;
-    a.m = m;
     a.n = w->n_out;
     a.k = w->k_in;
     a.main = w->dev.main;
     a.ovf = w->dev.ovf;
+    a.main_bytes = (uint32_t)ti.main.size();
+    a.ovf_bytes = (uint32_t)ti.ovf.size();
     a.ovf_ptr = w->dev.ovf_ptr;
     a.w_scale = w->dev.w_scale;
     a.bias = w->dev.bias;
@@ -639,33 +818,51 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int64_t m, f
     a.inv_so = inv_so;
     a.n_tiles = ti.n_tiles;
     a.n_win = ti.n_win;
-    const bool vec = (w->k_in % 16 == 0) && ((reinterpret_cast<uintptr_t>(x) & 15) == 0);
-    const TileCfg cfg = choose_cfg(m, w);
-    a.n_cgroups = (ti.n_tiles + cfg.nt() - 1) / cfg.nt();
-    const int64_t mt = (m + cfg.tm() - 1) / cfg.tm();
-    const int64_t nwg = mt * a.n_cgroups;
-    if (nwg > 0x7fffffff) {
-        set_error("m_tokens too large for one launch");
-        return SL_ERR_UNSUPPORTED;
-    }
     hipStream_t s = static_cast<hipStream_t>(stream);
-    switch (kind) {
-    case SL_EPI_ACC_I32: return launch_vec<SL_EPI_ACC_I32>(a, nullptr, cfg, nwg, s, vec);
-    case SL_EPI_F32: return launch_vec<SL_EPI_F32>(a, nullptr, cfg, nwg, s, vec);
-    case SL_EPI_F32_GELU: return launch_vec<SL_EPI_F32_GELU>(a, nullptr, cfg, nwg, s, vec);
-    case SL_EPI_I8: return launch_vec<SL_EPI_I8>(a, nullptr, cfg, nwg, s, vec);
-    default: {
+
+    GeluArg ga;
+    int32_t run_kind = kind;
+    if (kind == SL_EPI_I8_GELU) {
         std::shared_ptr<const GeluTable> tab = gelu_table(inv_so);
-        if (!tab->ok) return launch_vec<kEpiI8GeluErf>(a, nullptr, cfg, nwg, s, vec);
-        GeluArg ga;
-        ga.hinv = tab->hinv;
-        ga.off = tab->off;
-        ga.nc = tab->nc;
-        ga.pad = 0;
-        memcpy(ga.cell, tab->cell, sizeof(ga.cell));
-        return launch_vec<SL_EPI_I8_GELU>(a, &ga, cfg, nwg, s, vec);
+        if (tab->ok) {
+            ga.hinv = tab->hinv;
+            ga.off = tab->off;
+            ga.nc = tab->nc;
+            ga.pad = 0;
+            memcpy(ga.cell, tab->cell, sizeof(ga.cell));
+        } else {
+            run_kind = kEpiI8GeluErf;
+        }
     }
+    // Token rows go through 32-bit buffer offsets: launch at most
+    // kMaxBufferBytes of X at a time (a multiple of every workgroup's tokens).
+    const int64_t out_bytes = (kind == SL_EPI_I8 || kind == SL_EPI_I8_GELU) ? 1 : 4;
+    const int64_t chunk = std::max<int64_t>(256, kMaxBufferBytes / std::max<int32_t>(w->k_in, 1) / 256 * 256);
+    for (int64_t t0 = 0; t0 < m; t0 += chunk) {
+        a.x = x + t0 * w->k_in;
+        a.y = static_cast<char *>(y) + t0 * w->n_out * out_bytes;
+        a.m = std::min(chunk, m - t0);
+        const bool vec = (w->k_in % 16 == 0) && ((reinterpret_cast<uintptr_t>(a.x) & 15) == 0);
+        const TileCfg cfg = choose_cfg(a.m, w);
+        a.n_cgroups = (ti.n_tiles + cfg.nt() - 1) / cfg.nt();
+        const int64_t mt = (a.m + cfg.tm() - 1) / cfg.tm();
+        const int64_t nwg = mt * a.n_cgroups;
+        if (nwg > 0x7fffffff) {
+            set_error("too many workgroups for one launch");
+            return SL_ERR_UNSUPPORTED;
+        }
+        sl_status st;
+        switch (run_kind) {
+        case SL_EPI_ACC_I32: st = launch_vec<SL_EPI_ACC_I32>(a, nullptr, cfg, nwg, s, vec); break;
+        case SL_EPI_F32: st = launch_vec<SL_EPI_F32>(a, nullptr, cfg, nwg, s, vec); break;
+        case SL_EPI_F32_GELU: st = launch_vec<SL_EPI_F32_GELU>(a, nullptr, cfg, nwg, s, vec); break;
+        case SL_EPI_I8: st = launch_vec<SL_EPI_I8>(a, nullptr, cfg, nwg, s, vec); break;
+        case SL_EPI_I8_GELU: st = launch_vec<SL_EPI_I8_GELU>(a, &ga, cfg, nwg, s, vec); break;
+        default: st = launch_vec<kEpiI8GeluErf>(a, nullptr, cfg, nwg, s, vec); break;
+        }
+        if (st != SL_OK) return st;
     }
+    return SL_OK;
 }
 
 sl_status launch_quantize(const float *x, int64_t n, float inv_scale, int8_t *q, void *stream)
