@@ -226,6 +226,15 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
     const int64_t m0 = mt * S::TM;
     const int32_t tile0 = cg * S::NT;
     const int32_t ntl = min(S::NT, a.n_tiles - tile0);
+    // Workgroups walk the windows from different starting points (integer
+    // accumulation does not depend on the order), so the workgroups that share
+    // an input or weight line fetch it at different times: the first one
+    // misses in L2, the others hit.
+    const int rot = (int)((work * 7) % a.n_win);
+    auto phys = [&](int w) {
+        const int p = min(w, a.n_win - 1) + rot;
+        return p >= a.n_win ? p - a.n_win : p;
+    };
     const int tid = threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int lane = tid & 63;
@@ -422,8 +431,9 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
             // windows' copies still in flight
             __builtin_amdgcn_s_barrier();
             asm volatile("" ::: "memory");
-            // past the end: a harmless repeat keeps the copy count fixed
-            const int wcp = min(w + D - 1, a.n_win - 1);
+            // past the end: a harmless repeat (of the last window in this
+            // workgroup's order) keeps the copy count fixed
+            const int wcp = phys(w + D - 1);
             const uint2 o = om_at(wcp);
             int8_t *nb = smem + ((u + D - 1) % D) * S::BUF;
 #pragma unroll
@@ -432,7 +442,7 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
         };
 #pragma unroll
         for (int d = 0; d < D - 1; ++d) {
-            const int wd = min(d, a.n_win - 1);
+            const int wd = phys(d);
             const uint2 od = om_at(wd);
 #pragma unroll
             for (int k = 0; k < S::COPIES; ++k) copy(k, wd, smem + d * S::BUF, od.x, od.y);
@@ -467,7 +477,7 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
         lane * 128 < ntl * kOpBytes ? (uint32_t)(tile0 * kOpBytes + lane * 128) : kOob;
     lds_void *pf_dst = (lds_void *)(smem + S::LDS);
     auto prefetch = [&](int w) {
-        const int wp = min(w, a.n_win - 1);
+        const int wp = phys(w);
         if (wave < XI) {
             __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, pf_dst, 4, pf_xoff, (uint32_t)(wp * kWin), 0, 0);
         } else if (wave == XI) {
@@ -488,7 +498,7 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
         Ops &nxt = ops[(u + 1) & 1];
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
-        const uint32_t mask_n2 = om_at(w + 2).x;
+        const uint32_t mask_n2 = om_at(phys(w + 2)).x;
         if constexpr (kPrefetchAhead > 0) prefetch(w + kPrefetchAhead);
         const int8_t *nb = smem + ((u + 1) % D) * S::BUF;
         // Main part: window w+1's main operand reads and window w's main
@@ -529,8 +539,8 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
         for (int d = D - 1; d < kPrefetchAhead; ++d) prefetch(d);
     __builtin_amdgcn_s_barrier();  // window 0 has landed
     asm volatile("" ::: "memory");
-    mask_w = om_at(0).x;
-    mask_n = om_at(1).x;
+    mask_w = om_at(phys(0)).x;
+    mask_n = om_at(phys(1)).x;
     read_ops(ops[0], smem, mask_w);
     {
         int w = 0;
