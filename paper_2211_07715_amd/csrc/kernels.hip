@@ -52,12 +52,9 @@ constexpr int kXcds = 8;              // accelerator complex dies, each with its
 constexpr uint32_t kOob = 0x80000000u;
 constexpr int32_t kRsrcWord3 = 0x00020000;
 constexpr int64_t kMaxBufferBytes = 0x7ff00000;  // per launch: token chunk bytes and weight image
-// L2 prefetch: the compute waves touch every 128-byte line of the window
-// kPrefetchAhead windows ahead with 4-byte buffer loads into a scratch LDS
-// area (kPrefetchLds bytes, never read), so the copies of that window later
-// hit L2 instead of waiting on memory.
-constexpr int kPrefetchAhead = 0;
-constexpr int kPrefetchLds = 256;
+// per workgroup, ahead of the windows: its output channels' weight scales
+// and biases (one 1 KiB copy each, read by the epilogue from LDS)
+constexpr int kVecLds = 2048;
 constexpr size_t kLdsMax = 160 * 1024; // LDS per workgroup on gfx950
 
 #define HIP_TRY(expr)                                                                     \
@@ -246,11 +243,14 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
     const int wm = wave % WM, wn = (wave / WM) % WN;
     const size_t pstride = (size_t)a.n_tiles + 1;
 
-    // per window: bit j set if tile tile0 + j has an overflow operand, and the
-    // index of the workgroup's first overflow operand of the window (one
-    // round of independent loads per thread)
-    uint2 *om = reinterpret_cast<uint2 *>(smem + S::LDS + kPrefetchLds);
-    for (int w = tid; w < a.n_win; w += S::NTHG) {
+    // Built by the compute waves while the copy waves start the first
+    // windows: per window, bit j set if tile tile0 + j has an overflow
+    // operand, and the index of the workgroup's first overflow operand of the
+    // window (one round of independent loads per thread).
+    const float *vec_sw = reinterpret_cast<const float *>(smem + S::LDS);
+    const float *vec_b = reinterpret_cast<const float *>(smem + S::LDS + 1024);
+    uint2 *om = reinterpret_cast<uint2 *>(smem + S::LDS + kVecLds);
+    for (int w = copier ? a.n_win : tid; w < a.n_win; w += S::NTH) {
         const uint32_t *p = a.ovf_ptr + (size_t)w * pstride + tile0;
         uint32_t v[S::NT + 1];
 #pragma unroll
@@ -260,10 +260,10 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
         for (int j = 0; j < S::NT; ++j) mask |= (j < ntl && v[j + 1] > v[j] ? 1u : 0u) << j;
         om[w] = make_uint2(mask, v[0]);
     }
-    GeluCell *tab = reinterpret_cast<GeluCell *>(smem + S::LDS + kPrefetchLds + ((a.n_win * 8 + 15) & ~15));
+    GeluCell *tab = reinterpret_cast<GeluCell *>(smem + S::LDS + kVecLds + ((a.n_win * 8 + 15) & ~15));
     float hinv = 0.0f, eoff = 0.0f, cmax = 0.0f;
     if constexpr (KIND == SL_EPI_I8_GELU) {
-        for (int u = tid; u < ep->nc; u += S::NTHG) tab[u] = ep->cell[u];
+        for (int u = copier ? ep->nc : tid; u < ep->nc; u += S::NTH) tab[u] = ep->cell[u];
         hinv = ep->hinv;
         eoff = ep->off;
         cmax = (float)(ep->nc - 1);
@@ -412,20 +412,56 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
     // means every compute wave has finished reading window w-1's buffer
     // (those reads were consumed by the previous step's matrix instructions).
     static_assert(D >= 3, "the pipeline reads one window ahead of the one it multiplies");
+    static_assert(D <= 4, "the step-0 wait assumes at most one window issued after window 1 in the prologue");
     constexpr int U = D % 2 ? 2 * D : D;  // unroll: buffer index and register set both repeat
 
-    __syncthreads();  // overflow masks and epilogue table visible
+    // Prologue. The copy waves start the weight scales and biases, and the
+    // token rows and main operands of windows 0..D-2 (none of which need the
+    // overflow table); the compute waves build the overflow table and the
+    // epilogue table. A bare barrier (A) publishes the tables, then the copy
+    // waves add the overflow operands of windows 0..D-2 and wait for window
+    // 0; a second barrier (B) publishes it.
+    if (copier) {
+        if (pw == 0 && KIND != SL_EPI_ACC_I32) {
+            static_assert(S::NT * 16 * 4 <= 1024, "scales of one workgroup fit one copy");
+            const __amdgpu_buffer_rsrc_t sr =
+                __builtin_amdgcn_make_buffer_rsrc((void *)a.w_scale, 0, a.n * 4, kRsrcWord3);
+            const __amdgpu_buffer_rsrc_t br = __builtin_amdgcn_make_buffer_rsrc((void *)a.bias, 0, a.n * 4, kRsrcWord3);
+            const uint32_t vo = lane < S::NT * 4 ? (uint32_t)((tile0 * 16 + lane * 4) * 4) : kOob;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(sr, (lds_void *)(smem + S::LDS), 16, vo, 0, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(br, (lds_void *)(smem + S::LDS + 1024), 16, vo, 0, 0, 0);
+        }
+#pragma unroll
+        for (int d = 0; d < D - 1; ++d) {
+#pragma unroll
+            for (int k = 0; k < S::CX + S::CA; ++k) copy(k, phys(d), smem + d * S::BUF, 0u, 0u);
+            stage_rows(phys(d), smem + d * S::BUF);
+        }
+        __builtin_amdgcn_s_barrier();  // (A)
+        asm volatile("" ::: "memory");
+    } else {
+        __builtin_amdgcn_s_waitcnt(0);  // the tables' LDS stores are done
+        __builtin_amdgcn_s_barrier();   // (A)
+        asm volatile("" ::: "memory");
+    }
     if (lane < a.n_win) {
         om_lx = om[lane].x;
         om_ly = om[lane].y;
     }
     if (copier) {
         auto cstep = [&](int w, int u) {
+            // window w+1 has landed once the copies issued after its last one
+            // are all that is outstanding: at step 0 the overflow copies of
+            // windows 2..D-2 (prologue order), later the D-3 windows after it
             if (w + 1 < a.n_win) {
-                if constexpr (VEC)
-                    wait_vmcnt_le<(D - 3) * S::COPIES>();
-                else
+                if constexpr (VEC) {
+                    if (w == 0)
+                        wait_vmcnt_le<(D - 3) * S::CA>();
+                    else
+                        wait_vmcnt_le<(D - 3) * S::COPIES>();
+                } else {
                     __builtin_amdgcn_s_waitcnt(0);
+                }
             }
             // a bare barrier: __syncthreads() would also wait for the later
             // windows' copies still in flight
@@ -442,17 +478,15 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
         };
 #pragma unroll
         for (int d = 0; d < D - 1; ++d) {
-            const int wd = phys(d);
-            const uint2 od = om_at(wd);
+            const uint2 od = om_at(phys(d));
 #pragma unroll
-            for (int k = 0; k < S::COPIES; ++k) copy(k, wd, smem + d * S::BUF, od.x, od.y);
-            stage_rows(wd, smem + d * S::BUF);
+            for (int k = S::CX + S::CA; k < S::COPIES; ++k) copy(k, phys(d), smem + d * S::BUF, od.x, od.y);
         }
         if constexpr (VEC)
-            wait_vmcnt_le<(D - 2) * S::COPIES>();
+            wait_vmcnt_le<(D - 2) * S::CA>();  // window 0 (and the scales) landed
         else
             __builtin_amdgcn_s_waitcnt(0);
-        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_s_barrier();  // (B)
         asm volatile("" ::: "memory");
         int w = 0;
         for (; w + U <= a.n_win; w += U) {
@@ -466,30 +500,7 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
         return;
     }
 
-    // compute waves. Prefetch duty per wave: waves 0..XI-1 the token rows
-    // (64 per wave), the next wave the main operands, the one after the
-    // overflow operands of the workgroup's tiles.
-    constexpr int XI = (S::TM + 63) / 64;
-    static_assert(XI + 2 <= S::NW, "not enough compute waves for the prefetch duties");
-    const int pf_row = wave * 64 + lane;
-    const uint32_t pf_xoff = (wave < XI && pf_row < S::TM && m0 + pf_row < a.m) ? (uint32_t)((m0 + pf_row) * a.k) : kOob;
-    const uint32_t pf_moff =
-        lane * 128 < ntl * kOpBytes ? (uint32_t)(tile0 * kOpBytes + lane * 128) : kOob;
-    lds_void *pf_dst = (lds_void *)(smem + S::LDS);
-    auto prefetch = [&](int w) {
-        const int wp = phys(w);
-        if (wave < XI) {
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, pf_dst, 4, pf_xoff, (uint32_t)(wp * kWin), 0, 0);
-        } else if (wave == XI) {
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(mr, pf_dst, 4, pf_moff, (uint32_t)wp * wstride, 0, 0);
-        } else if (wave == XI + 1) {
-            const uint2 o = om_at(wp);
-            const uint32_t nov = __builtin_popcount(o.x);
-            const uint32_t off = lane * 128u < nov * (uint32_t)kOpBytes ? o.y * (uint32_t)kOpBytes + lane * 128u : kOob;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(orc, pf_dst, 4, off, 0, 0, 0);
-        }
-    };
-
+    // compute waves
     // mask_w: overflow mask of window w (its operands are in ops[u & 1]);
     // mask_n: of window w+1
     uint32_t mask_w, mask_n;
@@ -499,7 +510,6 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
         const uint32_t mask_n2 = om_at(phys(w + 2)).x;
-        if constexpr (kPrefetchAhead > 0) prefetch(w + kPrefetchAhead);
         const int8_t *nb = smem + ((u + 1) % D) * S::BUF;
         // Main part: window w+1's main operand reads and window w's main
         // matrix instructions, one after the other, so that a read waiting
@@ -535,9 +545,7 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
         mask_w = mask_n;
         mask_n = mask_n2;
     };
-    if constexpr (kPrefetchAhead > 0)
-        for (int d = D - 1; d < kPrefetchAhead; ++d) prefetch(d);
-    __builtin_amdgcn_s_barrier();  // window 0 has landed
+    __builtin_amdgcn_s_barrier();  // (B): window 0 has landed
     asm volatile("" ::: "memory");
     mask_w = om_at(phys(0)).x;
     mask_n = om_at(phys(1)).x;
@@ -563,8 +571,9 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
         if (ch0 >= a.n) continue;  // block-rows past n_out in the last tile
         float s[4] = {0, 0, 0, 0}, bb4[4] = {0, 0, 0, 0};
         if constexpr (KIND != SL_EPI_ACC_I32) {
-            const float4 sw = *reinterpret_cast<const float4 *>(a.w_scale + ch0);
-            const float4 bb = *reinterpret_cast<const float4 *>(a.bias + ch0);
+            const int lc = (wn * CT + c) * kTileN + 4 * (lane >> 4);  // channel within the workgroup
+            const float4 sw = *reinterpret_cast<const float4 *>(vec_sw + lc);
+            const float4 bb = *reinterpret_cast<const float4 *>(vec_b + lc);
             s[0] = a.sx * sw.x;
             s[1] = a.sx * sw.y;
             s[2] = a.sx * sw.z;
@@ -727,7 +736,7 @@ static sl_status launch_cfg(const LinearArgs &a, const GeluArg *ep, int64_t nwg,
         HIP_TRY(hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, kLdsMax));
         attr_done = true;
     }
-    const size_t lds = (size_t)S::LDS + kPrefetchLds + (((size_t)a.n_win * 8 + 15) & ~(size_t)15) +
+    const size_t lds = (size_t)S::LDS + kVecLds + (((size_t)a.n_win * 8 + 15) & ~(size_t)15) +
                        (KIND == SL_EPI_I8_GELU ? kGeluCells * sizeof(GeluCell) : 0);
     if (lds > kLdsMax) {
         set_error("k_in too large for this workgroup shape's per-window table");
