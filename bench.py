@@ -21,7 +21,10 @@ buffers) between two events, which gives its average launch duration.
 algorithmic bytes (X + Y + canonical packed W + scales) per launch divided by
 that duration; ``traffic`` is the counter-measured bytes per launch from
 profiles/traffic.json when that file was taken on the current kernel source.
-``cpu_baseline`` times the CPU oracle on the same step.
+``cpu_baseline`` times the CPU oracle on the same step. ``layer_latency``
+gives the DistilBERT-layer latency: one layer's four linears at batch 32 x
+seq 128 and the 6-layer stack at batch 1 x seq 128 (80 % sparsity, warm,
+host-launched and replayed from a HIP graph).
 
 Launch order (used to match profiler dispatches to ops): one step per buffer
 set (set-up), W warm-up steps, K timed steps, then KERNEL_REPS launches of
@@ -62,6 +65,84 @@ def algorithmic_bytes(m, n, k, nnzb, out_bytes):
     return m * k + m * n * out_bytes + nnzb * 6 + (n // 4 + 1) * 4 + 8 * n
 
 
+def chain_latency(torch, sl, wk, name, calib, stream, dev, reps=200, warmup=20):
+    """Latency of a workload's chain of linears (inputs resident, buffers
+    reused: a warm, latency-oriented figure). Returns host-launched time per
+    chain and per layer, and the same chain replayed from a HIP graph (after
+    checking that a replay reproduces the eagerly computed outputs)."""
+    wl = wk.workloads()[name]
+    ops = wk.op_list(wl)
+    packed, bufs, seeded, kinds = {}, {}, {}, {}
+    for layer, op in ops:
+        key = f"L{layer}.{op.name}"
+        wd = wk.op_weight(wl, layer, op)
+        packed[key] = sl.PackedWeight.pack(wd["w"], wd["sw"], wd["b"])
+        kinds[key] = sl.EPI_BY_NAME[wl.op_kind(layer, op)]
+        dt = torch.int8 if kinds[key] in (3, 4) else (torch.int32 if kinds[key] == 0 else torch.float32)
+        bufs[key] = torch.empty((wl.m, op.n_out), dtype=dt, device=dev)
+        if wl.op_src(layer, op) == "seeded":
+            seeded[key] = torch.from_numpy(wk.op_seeded_x(wl, layer, op)).to(dev)
+
+    def chain():
+        st = torch.cuda.current_stream()  # the capture stream while a graph is recorded
+        for layer, op in ops:
+            key = f"L{layer}.{op.name}"
+            src = wl.op_src(layer, op)
+            if src == "seeded":
+                xin, xs = seeded[key], float(wk.SX)
+            else:
+                xin, xs = bufs[src], float(calib[src])
+            packed[key].run(xin, xs, kinds[key], out_scale=float(calib.get(key, 1.0)), out=bufs[key], stream=st)
+
+    for _ in range(warmup):
+        chain()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        chain()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    eager_us = e0.elapsed_time(e1) / reps * 1e3
+    out = {"workload": f"{wl.name}: {wl.notes}", "m_tokens": wl.m, "layers": wl.layers, "linears": len(ops),
+           "chain_us": round(eager_us, 2), "per_layer_us": round(eager_us / wl.layers, 2)}
+    ref = {k: v.clone() for k, v in bufs.items()}
+    try:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            chain()
+        ok = True
+        for _ in range(3):
+            for v in bufs.values():
+                v.zero_()
+            g.replay()
+            torch.cuda.synchronize()
+            ok = ok and all(torch.equal(bufs[k], ref[k]) for k in bufs)
+            chain()  # eager work between replays
+            torch.cuda.synchronize()
+        if ok:
+            for _ in range(warmup):
+                g.replay()
+            torch.cuda.synchronize()
+            e0.record(stream)
+            for _ in range(reps):
+                g.replay()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            gus = e0.elapsed_time(e1) / reps * 1e3
+            out["graph_chain_us"] = round(gus, 2)
+            out["graph_per_layer_us"] = round(gus / wl.layers, 2)
+        else:
+            out["graph_chain_us"] = None
+            out["graph_note"] = "graph replay did not reproduce the eager outputs"
+    except Exception as e:  # graph capture unavailable: report the eager figure only
+        out["graph_chain_us"] = None
+        out["graph_note"] = f"graph capture failed: {type(e).__name__}"
+    for w in packed.values():
+        w.free()
+    return out
+
+
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
@@ -70,6 +151,7 @@ def parse():
     p.add_argument("--workload", default="c1")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--cpu-seconds", type=float, default=10.0)
+    p.add_argument("--no-latency", action="store_true", help="skip the DistilBERT-layer latency legs")
     p.add_argument("--copy-calib", action="store_true",
                    help="after the timed steps, run a plain elementwise copy of COPY_CALIB_BYTES three times "
                         "(the reference kernel that scales the HBM byte counters)")
@@ -213,6 +295,16 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    # ---- DistilBERT-layer latency: one layer's four linears at batch 32 x
+    # seq 128, and the 6-layer stack at batch 1 x seq 128 (80 % sparsity)
+    latency = None
+    if not args.no_latency:
+        with open(os.path.join(ROOT, "tests", "golden", "calibration.json")) as f:
+            calib_all = json.load(f)
+        latency = {}
+        for name, label in (("c2", "bs32_seq128_80pct_layer"), ("c3_seq128_s80", "bs1_seq128_80pct_6layers")):
+            latency[label] = chain_latency(torch, sl, wk, name, calib_all[name], stream, dev)
+
     # ---- CPU oracle baseline on the same step (bounded by time)
     cpu = None
     if not args.no_cpu:
@@ -257,6 +349,7 @@ def main():
         "kernels": kernels,
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "layer_latency": latency,
     }
     print(json.dumps(line), flush=True)
 
