@@ -76,7 +76,7 @@ struct LinearArgs {
     const int8_t *ovf;
     uint32_t main_bytes;  // image sizes: the range of the buffer loads
     uint32_t ovf_bytes;
-    const uint32_t *ovf_ptr;
+    const uint32_t *om;  // overflow table of this launch's tile-group size, [n_win][n_cgroups][2]
     const float *w_scale;
     const float *bias;
     float sx;
@@ -209,6 +209,25 @@ __device__ __forceinline__ void wait_vmcnt_le()
     __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
+// Copy waves, start of step w: wait until window w+1 has landed. The copies
+// issued after window w+1's last copy may stay outstanding: in the prologue
+// order (token rows and main operands of windows 0..D-2, then their overflow
+// operands) that is the overflow copies of windows w+2..D-2 plus the windows
+// copied in steps 0..w-1, later the D-3 windows copied after it.
+template <int D, int CA, int COPIES, int I = 0>
+__device__ __forceinline__ void wait_window_landed(int w)
+{
+    if constexpr (I < D - 3) {
+        if (w == I) {
+            wait_vmcnt_le<(D - 3 - I) * CA + I * COPIES>();
+            return;
+        }
+        wait_window_landed<D, CA, COPIES, I + 1>(w);
+    } else {
+        wait_vmcnt_le<(D - 3) * COPIES>();
+    }
+}
+
 // VEC: X rows are 16-byte aligned and k % 16 == 0, so token rows are copied
 // to LDS with 16-byte direct loads; otherwise they are staged byte by byte.
 template <int KIND, int ST, int CT, int WM, int WN, int D, bool VEC>
@@ -241,26 +260,10 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
     const bool copier = wave >= S::NW;
     const int pw = copier ? wave - S::NW : 0;  // copy-wave index
     const int wm = wave % WM, wn = (wave / WM) % WN;
-    const size_t pstride = (size_t)a.n_tiles + 1;
 
-    // Built by the compute waves while the copy waves start the first
-    // windows: per window, bit j set if tile tile0 + j has an overflow
-    // operand, and the index of the workgroup's first overflow operand of the
-    // window (one round of independent loads per thread).
     const float *vec_sw = reinterpret_cast<const float *>(smem + S::LDS);
     const float *vec_b = reinterpret_cast<const float *>(smem + S::LDS + 1024);
-    uint2 *om = reinterpret_cast<uint2 *>(smem + S::LDS + kVecLds);
-    for (int w = copier ? a.n_win : tid; w < a.n_win; w += S::NTH) {
-        const uint32_t *p = a.ovf_ptr + (size_t)w * pstride + tile0;
-        uint32_t v[S::NT + 1];
-#pragma unroll
-        for (int j = 0; j <= S::NT; ++j) v[j] = j <= ntl ? p[j] : 0u;
-        uint32_t mask = 0;
-#pragma unroll
-        for (int j = 0; j < S::NT; ++j) mask |= (j < ntl && v[j + 1] > v[j] ? 1u : 0u) << j;
-        om[w] = make_uint2(mask, v[0]);
-    }
-    GeluCell *tab = reinterpret_cast<GeluCell *>(smem + S::LDS + kVecLds + ((a.n_win * 8 + 15) & ~15));
+    GeluCell *tab = reinterpret_cast<GeluCell *>(smem + S::LDS + kVecLds);
     float hinv = 0.0f, eoff = 0.0f, cmax = 0.0f;
     if constexpr (KIND == SL_EPI_I8_GELU) {
         for (int u = copier ? ep->nc : tid; u < ep->nc; u += S::NTH) tab[u] = ep->cell[u];
@@ -389,16 +392,14 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
         for (int c = 0; c < CT; ++c)
             if ((mask >> (wn * CT + c)) & 1u) read_ovf(r, b, c);  // (ao, io used only under the same condition)
     };
-    // overflow entry of window w (clamped to the last window). Up to 64
-    // windows the entries sit one per lane in registers and a lane read
-    // fetches one without an LDS round trip.
-    uint32_t om_lx = 0, om_ly = 0;
+    // overflow entry (mask, first index) of window w for this workgroup's
+    // tiles, from the table built at packing; the address is uniform, so it is
+    // a scalar load, counted apart from the copies
+    typedef const __attribute__((address_space(4))) uint64_t *const_u64_ptr;
+    const const_u64_ptr omt = (const_u64_ptr)(a.om) + cg;
     auto om_at = [&](int w) {
-        const int wc = min(w, a.n_win - 1);
-        if (a.n_win <= 64)
-            return make_uint2((uint32_t)__builtin_amdgcn_readlane((int)om_lx, wc),
-                              (uint32_t)__builtin_amdgcn_readlane((int)om_ly, wc));
-        return make_uint2(__builtin_amdgcn_readfirstlane(om[wc].x), __builtin_amdgcn_readfirstlane(om[wc].y));
+        const uint64_t v = omt[(size_t)w * a.n_cgroups];
+        return make_uint2((uint32_t)v, (uint32_t)(v >> 32));
     };
 
     // Software pipeline over windows, one barrier per window. In step w
@@ -412,15 +413,15 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
     // means every compute wave has finished reading window w-1's buffer
     // (those reads were consumed by the previous step's matrix instructions).
     static_assert(D >= 3, "the pipeline reads one window ahead of the one it multiplies");
-    static_assert(D <= 4, "the step-0 wait assumes at most one window issued after window 1 in the prologue");
+    static_assert((D - 2) * S::COPIES < 64, "outstanding copies must fit the 6-bit vector-memory counter");
     constexpr int U = D % 2 ? 2 * D : D;  // unroll: buffer index and register set both repeat
 
     // Prologue. The copy waves start the weight scales and biases, and the
-    // token rows and main operands of windows 0..D-2 (none of which need the
-    // overflow table); the compute waves build the overflow table and the
-    // epilogue table. A bare barrier (A) publishes the tables, then the copy
-    // waves add the overflow operands of windows 0..D-2 and wait for window
-    // 0; a second barrier (B) publishes it.
+    // token rows and main operands of windows 0..D-2, while their overflow
+    // entries load; the compute waves fill the epilogue table. A bare barrier
+    // (A) publishes the table, then the copy waves add the overflow operands
+    // of windows 0..D-2 and wait for window 0; a second barrier (B) publishes
+    // it.
     if (copier) {
         if (pw == 0 && KIND != SL_EPI_ACC_I32) {
             static_assert(S::NT * 16 * 4 <= 1024, "scales of one workgroup fit one copy");
@@ -440,28 +441,17 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
         __builtin_amdgcn_s_barrier();  // (A)
         asm volatile("" ::: "memory");
     } else {
-        __builtin_amdgcn_s_waitcnt(0);  // the tables' LDS stores are done
+        __builtin_amdgcn_s_waitcnt(0);  // the epilogue table's LDS stores are done
         __builtin_amdgcn_s_barrier();   // (A)
         asm volatile("" ::: "memory");
     }
-    if (lane < a.n_win) {
-        om_lx = om[lane].x;
-        om_ly = om[lane].y;
-    }
     if (copier) {
         auto cstep = [&](int w, int u) {
-            // window w+1 has landed once the copies issued after its last one
-            // are all that is outstanding: at step 0 the overflow copies of
-            // windows 2..D-2 (prologue order), later the D-3 windows after it
             if (w + 1 < a.n_win) {
-                if constexpr (VEC) {
-                    if (w == 0)
-                        wait_vmcnt_le<(D - 3) * S::CA>();
-                    else
-                        wait_vmcnt_le<(D - 3) * S::COPIES>();
-                } else {
+                if constexpr (VEC)
+                    wait_window_landed<D, S::CA, S::COPIES>(w);
+                else
                     __builtin_amdgcn_s_waitcnt(0);
-                }
             }
             // a bare barrier: __syncthreads() would also wait for the later
             // windows' copies still in flight
@@ -651,6 +641,22 @@ sl_status check_device_arch(int *device)
     return SL_OK;
 }
 
+// Workgroup shapes (ST, CT, WM, WN, D): (16*ST*WM) tokens x (16*CT*WN)
+// channels, D windows in flight.
+struct TileCfg {
+    int st, ct, wm, wn, d;
+    int tm() const { return 16 * st * wm; }
+    int nt() const { return ct * wn; }
+};
+static const TileCfg kCfgs[] = {
+    {4, 3, 2, 2, 3},  // 128 x  96,  96 KiB LDS
+    {4, 3, 2, 2, 4},  // 128 x  96, 128 KiB
+    {2, 3, 2, 2, 3},  //  64 x  96,  72 KiB (two workgroups per CU)
+    {2, 3, 2, 2, 4},  //  64 x  96,  96 KiB
+    {1, 3, 2, 2, 6},  //  32 x  96, 120 KiB (few tokens: deep ring)
+    {1, 1, 2, 2, 8},  //  32 x  32,  96 KiB (few tokens: deep ring)
+};
+
 static size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
 sl_status upload_image(sl_packed_weight *w)
@@ -660,16 +666,45 @@ sl_status upload_image(sl_packed_weight *w)
         set_error("packed weight image over 2 GiB (n_out x k_in too large for one image)");
         return SL_ERR_UNSUPPORTED;
     }
+    // overflow tables, one per tile-group size of the shape table
+    std::vector<int> nts;
+    for (const TileCfg &c : kCfgs)
+        if (std::find(nts.begin(), nts.end(), c.nt()) == nts.end()) nts.push_back(c.nt());
+    if ((int)nts.size() > kMaxOmTables) {
+        set_error("internal: too many tile-group sizes");
+        return SL_ERR_UNSUPPORTED;
+    }
+    std::vector<std::vector<uint32_t>> oms(nts.size());
+    const size_t pstride = (size_t)ti.n_tiles + 1;
+    for (size_t i = 0; i < nts.size(); ++i) {
+        const int nt = nts[i];
+        const int ncg = (ti.n_tiles + nt - 1) / nt;
+        std::vector<uint32_t> &om = oms[i];
+        om.assign((size_t)ti.n_win * ncg * 2, 0u);
+        for (int wi = 0; wi < ti.n_win; ++wi)
+            for (int g = 0; g < ncg; ++g) {
+                const int t0 = g * nt, ntl = std::min(nt, ti.n_tiles - t0);
+                const uint32_t *pp = ti.ovf_ptr.data() + (size_t)wi * pstride + t0;
+                uint32_t mask = 0;
+                for (int j = 0; j < ntl; ++j) mask |= (pp[j + 1] > pp[j] ? 1u : 0u) << j;
+                om[((size_t)wi * ncg + g) * 2] = mask;
+                om[((size_t)wi * ncg + g) * 2 + 1] = pp[0];
+            }
+    }
     const size_t b_main = std::max<size_t>(ti.main.size(), 16);
     const size_t b_ovf = std::max<size_t>(ti.ovf.size(), 16);
-    const size_t b_ptr = ti.ovf_ptr.size() * sizeof(uint32_t);
     const size_t b_vec = (size_t)w->n_out * sizeof(float);
     const size_t o_main = 0;
     const size_t o_ovf = align256(o_main + b_main);
-    const size_t o_ptr = align256(o_ovf + b_ovf);
-    const size_t o_sw = align256(o_ptr + b_ptr);
+    const size_t o_sw = align256(o_ovf + b_ovf);
     const size_t o_b = align256(o_sw + b_vec);
-    const size_t total = align256(o_b + b_vec);
+    size_t o_end = align256(o_b + b_vec);
+    std::vector<size_t> o_om(nts.size());
+    for (size_t i = 0; i < nts.size(); ++i) {
+        o_om[i] = o_end;
+        o_end = align256(o_end + oms[i].size() * sizeof(uint32_t));
+    }
+    const size_t total = o_end;
     void *base = nullptr;
     hipError_t e = hipMalloc(&base, total);
     if (e != hipSuccess) {
@@ -682,12 +717,17 @@ sl_status upload_image(sl_packed_weight *w)
     w->on_device = true;  // from here on sparse_linear_free releases the memory
     if (!ti.main.empty()) HIP_TRY(hipMemcpy(p + o_main, ti.main.data(), ti.main.size(), hipMemcpyHostToDevice));
     if (!ti.ovf.empty()) HIP_TRY(hipMemcpy(p + o_ovf, ti.ovf.data(), ti.ovf.size(), hipMemcpyHostToDevice));
-    HIP_TRY(hipMemcpy(p + o_ptr, ti.ovf_ptr.data(), b_ptr, hipMemcpyHostToDevice));
     HIP_TRY(hipMemcpy(p + o_sw, w->w_scale.data(), b_vec, hipMemcpyHostToDevice));
     HIP_TRY(hipMemcpy(p + o_b, w->bias.data(), b_vec, hipMemcpyHostToDevice));
+    for (size_t i = 0; i < nts.size(); ++i) {
+        HIP_TRY(hipMemcpy(p + o_om[i], oms[i].data(), oms[i].size() * sizeof(uint32_t), hipMemcpyHostToDevice));
+        w->dev.om_nt[i] = nts[i];
+        w->dev.om[i] = reinterpret_cast<const uint32_t *>(p + o_om[i]);
+    }
+    w->dev.n_om = (int32_t)nts.size();
     w->dev.main = reinterpret_cast<const int8_t *>(p + o_main);
     w->dev.ovf = reinterpret_cast<const int8_t *>(p + o_ovf);
-    w->dev.ovf_ptr = reinterpret_cast<const uint32_t *>(p + o_ptr);
+    w->dev.ovf_ptr = nullptr;
     w->dev.w_scale = reinterpret_cast<const float *>(p + o_sw);
     w->dev.bias = reinterpret_cast<const float *>(p + o_b);
     return SL_OK;
@@ -706,22 +746,6 @@ void release_image(sl_packed_weight *w)
     w->on_device = false;
 }
 
-// Workgroup shapes (ST, CT, WM, WN, D): (16*ST*WM) tokens x (16*CT*WN)
-// channels, D windows in flight.
-struct TileCfg {
-    int st, ct, wm, wn, d;
-    int tm() const { return 16 * st * wm; }
-    int nt() const { return ct * wn; }
-};
-static const TileCfg kCfgs[] = {
-    {4, 3, 2, 2, 3},  // 128 x  96,  96 KiB LDS
-    {4, 3, 2, 2, 4},  // 128 x  96, 128 KiB
-    {2, 3, 2, 2, 3},  //  64 x  96,  72 KiB (two workgroups per CU)
-    {2, 3, 2, 2, 4},  //  64 x  96,  96 KiB
-    {1, 3, 2, 2, 3},  //  32 x  96,  60 KiB
-    {1, 1, 2, 2, 3},  //  32 x  32,  36 KiB
-};
-
 template <int KIND, int ST, int CT, int WM, int WN, int D, bool VEC>
 static sl_status launch_cfg(const LinearArgs &a, const GeluArg *ep, int64_t nwg, hipStream_t stream)
 {
@@ -736,12 +760,8 @@ static sl_status launch_cfg(const LinearArgs &a, const GeluArg *ep, int64_t nwg,
         HIP_TRY(hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, kLdsMax));
         attr_done = true;
     }
-    const size_t lds = (size_t)S::LDS + kVecLds + (((size_t)a.n_win * 8 + 15) & ~(size_t)15) +
-                       (KIND == SL_EPI_I8_GELU ? kGeluCells * sizeof(GeluCell) : 0);
-    if (lds > kLdsMax) {
-        set_error("k_in too large for this workgroup shape's per-window table");
-        return SL_ERR_UNSUPPORTED;
-    }
+    const size_t lds = (size_t)S::LDS + kVecLds + (KIND == SL_EPI_I8_GELU ? kGeluCells * sizeof(GeluCell) : 0);
+    static_assert(S::LDS + kVecLds + kGeluCells * sizeof(GeluCell) <= kLdsMax, "workgroup shape exceeds LDS");
     if constexpr (KIND == SL_EPI_I8_GELU)
         hipLaunchKernelGGL((sparse_linear_gelu_kernel<ST, CT, WM, WN, D, VEC>), dim3((uint32_t)nwg), dim3(S::NTHG),
                            lds, stream, a, *ep);
@@ -762,9 +782,9 @@ static sl_status launch_kind(const LinearArgs &a, const GeluArg *ep, TileCfg c, 
     SL_CFG(4, 3, 2, 2, 4)
     SL_CFG(2, 3, 2, 2, 3)
     SL_CFG(2, 3, 2, 2, 4)
-    SL_CFG(1, 3, 2, 2, 3)
+    SL_CFG(1, 3, 2, 2, 6)
 #undef SL_CFG
-    return launch_cfg<KIND, 1, 1, 2, 2, 3, VEC>(a, ep, nwg, stream);
+    return launch_cfg<KIND, 1, 1, 2, 2, 8, VEC>(a, ep, nwg, stream);
 }
 
 template <int KIND>
@@ -830,7 +850,6 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int64_t m, f
     a.ovf = w->dev.ovf;
     a.main_bytes = (uint32_t)ti.main.size();
     a.ovf_bytes = (uint32_t)ti.ovf.size();
-    a.ovf_ptr = w->dev.ovf_ptr;
     a.w_scale = w->dev.w_scale;
     a.bias = w->dev.bias;
     a.sx = sx;
@@ -864,6 +883,13 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int64_t m, f
         const bool vec = (w->k_in % 16 == 0) && ((reinterpret_cast<uintptr_t>(a.x) & 15) == 0);
         const TileCfg cfg = choose_cfg(a.m, w);
         a.n_cgroups = (ti.n_tiles + cfg.nt() - 1) / cfg.nt();
+        a.om = nullptr;
+        for (int i = 0; i < w->dev.n_om; ++i)
+            if (w->dev.om_nt[i] == cfg.nt()) a.om = w->dev.om[i];
+        if (!a.om) {
+            set_error("internal: no overflow table for the chosen workgroup shape");
+            return SL_ERR_UNSUPPORTED;
+        }
         const int64_t mt = (a.m + cfg.tm() - 1) / cfg.tm();
         const int64_t nwg = mt * a.n_cgroups;
         if (nwg > 0x7fffffff) {

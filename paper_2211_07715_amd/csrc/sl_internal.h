@@ -66,6 +66,12 @@ struct GeluTable {
 };
 std::shared_ptr<const GeluTable> gelu_table(float inv_so);
 
+// Per tile-group size nt (channel tiles per workgroup): for every window w and
+// group g, the pair (mask, first): bit j of mask set if tile g*nt + j has an
+// overflow operand in window w; first = index of the group's first overflow
+// operand of the window. Layout [n_win][n_groups][2] uint32.
+constexpr int kMaxOmTables = 4;
+
 struct DeviceImage {
     int device = -1;
     void *base = nullptr;  // one allocation holding everything below
@@ -74,6 +80,9 @@ struct DeviceImage {
     const uint32_t *ovf_ptr = nullptr;
     const float *w_scale = nullptr;
     const float *bias = nullptr;
+    int32_t n_om = 0;
+    int32_t om_nt[kMaxOmTables] = {};
+    const uint32_t *om[kMaxOmTables] = {};
     int64_t bytes = 0;
 };
 
