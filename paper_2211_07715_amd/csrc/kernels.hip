@@ -46,7 +46,8 @@ namespace sl {
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x8 __attribute__((ext_vector_type(8)));
 
-constexpr int kXcds = 8;              // accelerator complex dies, each with its own L2
+constexpr int kXcds = 8;  // accelerator complex dies, each with its own L2
+constexpr int kMaxDevices = 64;
 // Buffer-load offset past any buffer this library reads (all < 2 GiB): such
 // a lane reads zeros. Buffer word 3 for raw byte loads on gfx9.
 constexpr uint32_t kOob = 0x80000000u;
@@ -54,7 +55,9 @@ constexpr int32_t kRsrcWord3 = 0x00020000;
 constexpr int64_t kMaxBufferBytes = 0x7ff00000;  // per launch: token chunk bytes and weight image
 // per workgroup, ahead of the windows: its output channels' weight scales
 // and biases (one 1 KiB copy each, read by the epilogue from LDS)
-constexpr int kVecLds = 2048;
+constexpr int kVecLds = 512;  // a compute wave's weight scales and biases
+constexpr int kGeluLds = (kGeluCells * (int)sizeof(GeluCell) + 15) / 16 * 16;
+constexpr int kMaskLds = 256;  // the ring buffers' overflow masks
 constexpr size_t kLdsMax = 160 * 1024; // LDS per workgroup on gfx950
 
 #define HIP_TRY(expr)                                                                     \
@@ -84,6 +87,7 @@ struct LinearArgs {
     int32_t n_tiles;
     int32_t n_win;
     int32_t n_cgroups;  // channel groups of NT tiles
+    int64_t n_items;    // work items: token tiles x channel groups
 };
 
 // Workgroup shape: WM x WN waves; a wave owns ST 16-token subtiles x CT
@@ -105,7 +109,7 @@ struct Shape {
     static constexpr int CA = (NT * kOpPieces + NTH - 1) / NTH;  // copies per wave: each operand region
     static constexpr int XB = CX * NW * 1024;
     static constexpr int AB = CA * NTH * 16;
-    static constexpr int COPIES = CX + 2 * CA;  // per wave per window
+    static constexpr int COPIES = CX + 2 * CA + 1;  // per wave per window (+1: the overflow mask)
     static constexpr int BUF = XB + 2 * AB;
     static constexpr int LDS = D * BUF;
     static_assert(TM % 8 == 0, "token rows are copied 8 at a time");
@@ -209,11 +213,12 @@ __device__ __forceinline__ void wait_vmcnt_le()
     __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-// Copy waves, start of step w: wait until window w+1 has landed. The copies
-// issued after window w+1's last copy may stay outstanding: in the prologue
-// order (token rows and main operands of windows 0..D-2, then their overflow
-// operands) that is the overflow copies of windows w+2..D-2 plus the windows
-// copied in steps 0..w-1, later the D-3 windows copied after it.
+// Copy waves, start of step w: wait until element w+1 has landed. The copies
+// issued after element w+1's last copy may stay outstanding: in the prologue
+// order (token rows, main operands and overflow mask of elements 0..D-2, then
+// their overflow operands) that is the overflow copies of elements w+2..D-2
+// plus the elements copied in steps 0..w-1, later the D-3 elements copied
+// after it.
 template <int D, int CA, int COPIES, int I = 0>
 __device__ __forceinline__ void wait_window_landed(int w)
 {
@@ -228,6 +233,41 @@ __device__ __forceinline__ void wait_window_landed(int w)
     }
 }
 
+// The work items of one workgroup: slot, slot + G, slot + 2G, ... as token
+// tile mt, channel group cg and window rotation rot (items walk the windows
+// from different starting points; integer accumulation does not depend on
+// the order, and the workgroups that share an input or weight line then
+// fetch it at different times). next() advances by G without dividing.
+struct ItemIter {
+    int32_t mt, cg, rot;
+    int32_t dmt, dcg, drot;
+    int32_t n_cgroups, n_win;
+    __device__ static ItemIter start(int32_t slot, int32_t g, int32_t n_cgroups, int32_t n_win)
+    {
+        ItemIter it;
+        it.mt = slot / n_cgroups;
+        it.cg = slot - it.mt * n_cgroups;
+        it.rot = (int32_t)(((int64_t)slot * 7) % n_win);
+        it.dmt = g / n_cgroups;
+        it.dcg = g - it.dmt * n_cgroups;
+        it.drot = (int32_t)(((int64_t)g * 7) % n_win);
+        it.n_cgroups = n_cgroups;
+        it.n_win = n_win;
+        return it;
+    }
+    __device__ void next()
+    {
+        mt += dmt;
+        cg += dcg;
+        if (cg >= n_cgroups) {
+            cg -= n_cgroups;
+            ++mt;
+        }
+        rot += drot;
+        if (rot >= n_win) rot -= n_win;
+    }
+};
+
 // VEC: X rows are 16-byte aligned and k % 16 == 0, so token rows are copied
 // to LDS with 16-byte direct loads; otherwise they are staged byte by byte.
 template <int KIND, int ST, int CT, int WM, int WN, int D, bool VEC>
@@ -236,21 +276,6 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
     using S = Shape<ST, CT, WM, WN, D>;
     extern __shared__ __attribute__((aligned(16))) int8_t smem[];
 
-    const int64_t work = xcd_work_index(blockIdx.x, gridDim.x);
-    const int64_t mt = work / a.n_cgroups;
-    const int32_t cg = (int32_t)(work % a.n_cgroups);
-    const int64_t m0 = mt * S::TM;
-    const int32_t tile0 = cg * S::NT;
-    const int32_t ntl = min(S::NT, a.n_tiles - tile0);
-    // Workgroups walk the windows from different starting points (integer
-    // accumulation does not depend on the order), so the workgroups that share
-    // an input or weight line fetch it at different times: the first one
-    // misses in L2, the others hit.
-    const int rot = (int)((work * 7) % a.n_win);
-    auto phys = [&](int w) {
-        const int p = min(w, a.n_win - 1) + rot;
-        return p >= a.n_win ? p - a.n_win : p;
-    };
     const int tid = threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int lane = tid & 63;
@@ -261,9 +286,36 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
     const int pw = copier ? wave - S::NW : 0;  // copy-wave index
     const int wm = wave % WM, wn = (wave / WM) % WN;
 
-    const float *vec_sw = reinterpret_cast<const float *>(smem + S::LDS);
-    const float *vec_b = reinterpret_cast<const float *>(smem + S::LDS + 1024);
-    GeluCell *tab = reinterpret_cast<GeluCell *>(smem + S::LDS + kVecLds);
+    // Work items (token tile x channel group) of this workgroup: slot,
+    // slot + G, slot + 2G, ... below n_items, processed as one stream of
+    // (item, window) elements through the same LDS ring: the copies of the
+    // next item start while this item's last windows are multiplied, and the
+    // epilogue of an item overlaps the copies of the next.
+    const int32_t G = (int32_t)gridDim.x;
+    const int32_t slot = (int32_t)xcd_work_index(blockIdx.x, G);
+    const int n_my = (int)((a.n_items - slot + G - 1) / G);  // >= 1: the grid is at most n_items
+    const int64_t steps = (int64_t)n_my * a.n_win;
+    const ItemIter first = ItemIter::start(slot, G, a.n_cgroups, a.n_win);
+    auto phys = [&](const ItemIter &it, int w) {
+        const int p = w + it.rot;
+        return p >= a.n_win ? p - a.n_win : p;
+    };
+    // overflow entry (mask, first index) of physical window pwin for an
+    // item's tiles, from the table built at packing; the address is uniform,
+    // so it is a scalar load
+    typedef const __attribute__((address_space(4))) uint64_t *const_u64_ptr;
+    const const_u64_ptr omt = (const_u64_ptr)(a.om);
+    auto om_at = [&](const ItemIter &it, int pwin) {
+        const uint64_t v = omt[(size_t)pwin * a.n_cgroups + it.cg];
+        return make_uint2((uint32_t)v, (uint32_t)(v >> 32));
+    };
+    // overflow mask of each ring buffer's element, copied there from the
+    // table by each copy wave (omask[b * NW + copy wave]) with the element's
+    // operands
+    uint32_t *omask = reinterpret_cast<uint32_t *>(smem + S::LDS + (KIND == SL_EPI_I8_GELU ? kGeluLds : 0) +
+                                                   S::NW * kVecLds);
+
+    GeluCell *tab = reinterpret_cast<GeluCell *>(smem + S::LDS);
     float hinv = 0.0f, eoff = 0.0f, cmax = 0.0f;
     if constexpr (KIND == SL_EPI_I8_GELU) {
         for (int u = copier ? ep->nc : tid; u < ep->nc; u += S::NTH) tab[u] = ep->cell[u];
@@ -272,77 +324,208 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
         cmax = (float)(ep->nc - 1);
     }
 
-    i32x4 acc[CT][ST];
-#pragma unroll
-    for (int c = 0; c < CT; ++c)
-#pragma unroll
-        for (int s = 0; s < ST; ++s) acc[c][s] = i32x4{0, 0, 0, 0};
+    // Software pipeline over the element stream, one barrier per element. In
+    // step e
+    //  * the copy waves wait until element e+1 has landed, pass the barrier,
+    //    and start the copies of element e+D-1 into the buffer of element e-1;
+    //  * the compute waves pass the barrier, read element e+1's operands into
+    //    one register set while the matrix instructions of element e run from
+    //    the other, and after an item's last window run its epilogue.
+    // The barrier after the copy waves' wait makes element e+1 visible, and
+    // means every compute wave has finished reading element e-1's buffer
+    // (those reads were consumed by the previous step's matrix instructions).
+    static_assert(D >= 3, "the pipeline reads one element ahead of the one it multiplies");
+    static_assert((D - 2) * S::COPIES < 64, "outstanding copies must fit the 6-bit vector-memory counter");
 
-    // Copies go through buffer loads with a per-lane offset that is fixed
-    // for the launch (the window advance is a scalar offset), so a copy costs
-    // no vector instructions. A lane without data gets an offset past the
-    // buffer and copies zeros: rows past m, operand pieces past the
-    // workgroup's last tile, absent overflow operands.
-    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
-        (void *)a.x, 0, (int)min<int64_t>(a.m * a.k, kMaxBufferBytes), kRsrcWord3);
-    const __amdgpu_buffer_rsrc_t mr = __builtin_amdgcn_make_buffer_rsrc((void *)a.main, 0, (int)a.main_bytes, kRsrcWord3);
-    const __amdgpu_buffer_rsrc_t orc = __builtin_amdgcn_make_buffer_rsrc((void *)a.ovf, 0, (int)a.ovf_bytes, kRsrcWord3);
-    // token-row copy: row start + this lane's (permuted) piece of window 0,
-    // and the last offset inside the row (a ragged last window never reads
-    // past its row, so never past the buffer)
-    uint32_t xoff[S::CX], xlim[S::CX];
+    if (copier) {
+        // Copies go through buffer loads (a lane's offset plus a scalar window
+        // advance). A lane without data gets an offset past the buffer and
+        // copies zeros: rows past m, operand pieces past the item's last tile,
+        // absent overflow operands.
+        const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+            (void *)a.x, 0, (int)min<int64_t>(a.m * a.k, kMaxBufferBytes), kRsrcWord3);
+        const __amdgpu_buffer_rsrc_t mr =
+            __builtin_amdgcn_make_buffer_rsrc((void *)a.main, 0, (int)a.main_bytes, kRsrcWord3);
+        const __amdgpu_buffer_rsrc_t orc =
+            __builtin_amdgcn_make_buffer_rsrc((void *)a.ovf, 0, (int)a.ovf_bytes, kRsrcWord3);
+        const __amdgpu_buffer_rsrc_t omr =
+            __builtin_amdgcn_make_buffer_rsrc((void *)a.om, 0, a.n_win * a.n_cgroups * 8, kRsrcWord3);
+        const uint32_t wstride = (uint32_t)a.n_tiles * kOpBytes;  // main image bytes per window
+        // this lane's operand piece per operand copy
+        int32_t atile[S::CA], apiece16[S::CA];
 #pragma unroll
-    for (int i = 0; i < S::CX; ++i) {
-        const int r = ((i * S::NW + pw) * 64 + lane) / 8;
-        const bool in = r < S::TM && m0 + r < a.m;
-        xoff[i] = in ? (uint32_t)((m0 + r) * a.k + ((lane & 7) ^ xsw(r)) * 16) : kOob;
-        xlim[i] = in ? (uint32_t)((m0 + r) * a.k + a.k - 16) : kOob;
-    }
-    uint32_t aoff[S::CA];  // main operand piece of the workgroup's tile slice
-    int32_t atile[S::CA], apiece16[S::CA];
-#pragma unroll
-    for (int i = 0; i < S::CA; ++i) {
-        const int piece = (i * S::NW + pw) * 64 + lane;
-        atile[i] = piece / kOpPieces;
-        apiece16[i] = (piece - atile[i] * kOpPieces) * 16;
-        aoff[i] = atile[i] < ntl ? (uint32_t)((tile0 + atile[i]) * kOpBytes + apiece16[i]) : kOob;
-    }
-    const uint32_t wstride = (uint32_t)a.n_tiles * kOpBytes;  // main image bytes per window
-
-    // Copy k (0 <= k < COPIES) of window w into buffer b (global -> LDS,
-    // asynchronous): token rows, then main operands, then overflow operands
-    // into the slot of their tile. mask/olo: the window's overflow entry.
-    auto copy = [&](int k, int w, int8_t *b, uint32_t mask, uint32_t olo) {
-        if (k < S::CX) {
-            if constexpr (VEC)
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_void *)(b + (k * S::NW + pw) * 1024), 16,
-                                                         min(xoff[k] + (uint32_t)(w * kWin), xlim[k]), 0, 0, 0);
-        } else if (k < S::CX + S::CA) {
-            const int i = k - S::CX;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(mr, (lds_void *)(b + S::XB + (i * S::NW + pw) * 1024), 16,
-                                                     aoff[i], (uint32_t)w * wstride, 0, 0);
-        } else {
-            const int i = k - S::CX - S::CA;
-            const uint32_t t = (uint32_t)atile[i];
-            const bool has = t < 32u && ((mask >> t) & 1u);
-            const uint32_t rank = __builtin_popcount(mask & ((1u << (t & 31u)) - 1u));
-            const uint32_t o = has ? (olo + rank) * (uint32_t)kOpBytes + (uint32_t)apiece16[i] : kOob;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(orc, (lds_void *)(b + S::XB + S::AB + (i * S::NW + pw) * 1024),
-                                                     16, o, 0, 0, 0);
+        for (int i = 0; i < S::CA; ++i) {
+            const int piece = (i * S::NW + pw) * 64 + lane;
+            atile[i] = piece / kOpPieces;
+            apiece16[i] = (piece - atile[i] * kOpPieces) * 16;
         }
-    };
-    // without VEC the copy waves stage the token rows by ordinary stores
-    auto stage_rows = [&](int w, int8_t *b) {
-        if constexpr (!VEC) {
-            for (int u = tid - S::NTH; u < S::TM * kWin; u += S::NTH) {
-                const int r = u / kWin, c = u % kWin;
-                const int64_t tok = m0 + r;
-                const int32_t col = w * kWin + c;
-                b[r * kWin + (((c >> 4) ^ xsw(r)) << 4) + (c & 15)] =
-                    (tok < a.m && col < a.k) ? a.x[tok * a.k + col] : (int8_t)0;
+
+        // Element cursor: item ic (the k-th of this workgroup), window wc.
+        // Past the last element it stays on the last item and repeats its
+        // last window: a harmless copy that keeps the count fixed.
+        ItemIter ic = first;
+        int kc = 0, wc = 0;
+        auto cur_w = [&]() { return phys(ic, kc < n_my ? wc : a.n_win - 1); };
+        // this lane's offsets for the cursor's item: token-row copies (row
+        // start + permuted piece of window 0, and the last offset inside the
+        // row: a ragged last window never reads past its row, so never past
+        // the buffer) and main operand copies
+        uint32_t xoff[S::CX], xlim[S::CX], aoff[S::CA];
+        auto item_offsets = [&]() {
+            const int64_t m0 = (int64_t)ic.mt * S::TM;
+            const int32_t tile0 = ic.cg * S::NT;
+            const int32_t ntl = min(S::NT, a.n_tiles - tile0);
+#pragma unroll
+            for (int i = 0; i < S::CX; ++i) {
+                const int r = ((i * S::NW + pw) * 64 + lane) / 8;
+                const bool in = r < S::TM && m0 + r < a.m;
+                const uint32_t row = (uint32_t)((m0 + r) * a.k);
+                xoff[i] = in ? row + (uint32_t)(((lane & 7) ^ xsw(r)) * 16) : kOob;
+                xlim[i] = in ? row + (uint32_t)(a.k - 16) : kOob;
             }
+#pragma unroll
+            for (int i = 0; i < S::CA; ++i)
+                aoff[i] = atile[i] < ntl ? (uint32_t)((tile0 + atile[i]) * kOpBytes + apiece16[i]) : kOob;
+        };
+        auto advance = [&]() {
+            if (++wc == a.n_win) {
+                wc = 0;
+                if (++kc < n_my) {
+                    ic.next();
+                    item_offsets();
+                }
+            }
+        };
+        item_offsets();
+
+        // Copy k (0 <= k < COPIES) of the cursor's element (physical window w)
+        // into ring buffer bi (global -> LDS, asynchronous): token rows, main
+        // operands, the overflow mask (one lane, 4 bytes), then overflow
+        // operands into the slot of their tile. o: the element's overflow
+        // entry (only the overflow operand copies use it).
+        constexpr int KM = S::CX + S::CA;  // the mask copy
+        auto copy = [&](int k, int w, int bi, uint2 o) {
+            int8_t *b = smem + bi * S::BUF;
+            if (k < S::CX) {
+                if constexpr (VEC)
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_void *)(b + (k * S::NW + pw) * 1024), 16,
+                                                             min(xoff[k] + (uint32_t)(w * kWin), xlim[k]), 0, 0, 0);
+            } else if (k < KM) {
+                const int i = k - S::CX;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(mr, (lds_void *)(b + S::XB + (i * S::NW + pw) * 1024), 16,
+                                                         aoff[i], (uint32_t)w * wstride, 0, 0);
+            } else if (k == KM) {
+                if (lane == 0)
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(omr, (lds_void *)(omask + bi * S::NW + pw), 4,
+                                                             (uint32_t)(w * a.n_cgroups + ic.cg) * 8u, 0, 0, 0);
+            } else {
+                const int i = k - KM - 1;
+                const uint32_t mask = o.x, olo = o.y;
+                const uint32_t t = (uint32_t)atile[i];
+                const bool has = t < 32u && ((mask >> t) & 1u);
+                const uint32_t rank = __builtin_popcount(mask & ((1u << (t & 31u)) - 1u));
+                const uint32_t off = has ? (olo + rank) * (uint32_t)kOpBytes + (uint32_t)apiece16[i] : kOob;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    orc, (lds_void *)(b + S::XB + S::AB + (i * S::NW + pw) * 1024), 16, off, 0, 0, 0);
+            }
+        };
+        // without VEC the copy waves stage the token rows by ordinary stores
+        auto stage_rows = [&](int w, int8_t *b) {
+            if constexpr (!VEC) {
+                const int64_t m0 = (int64_t)ic.mt * S::TM;
+                for (int u = tid - S::NTH; u < S::TM * kWin; u += S::NTH) {
+                    const int r = u / kWin, c = u % kWin;
+                    const int64_t tok = m0 + r;
+                    const int32_t col = w * kWin + c;
+                    b[r * kWin + (((c >> 4) ^ xsw(r)) << 4) + (c & 15)] =
+                        (tok < a.m && col < a.k) ? a.x[tok * a.k + col] : (int8_t)0;
+                }
+            }
+        };
+
+        // Prologue: the overflow entries of elements 0..D-2 start loading, the
+        // token rows, main operands and overflow masks of those elements are
+        // copied, a bare barrier (A) publishes the epilogue table the compute
+        // waves filled, then the overflow operands follow; once element 0 has
+        // landed a second barrier (B) publishes it.
+        uint2 o[D - 1];
+        {
+            const ItemIter ic0 = ic;
+            const int kc0 = kc, wc0 = wc;
+#pragma unroll
+            for (int d = 0; d < D - 1; ++d) {
+                o[d] = om_at(ic, cur_w());
+                if (++wc == a.n_win) {
+                    wc = 0;
+                    if (++kc < n_my) ic.next();
+                }
+            }
+            ic = ic0;
+            kc = kc0;
+            wc = wc0;
         }
-    };
+        int wp[D - 1];
+#pragma unroll
+        for (int d = 0; d < D - 1; ++d) {
+            wp[d] = cur_w();
+#pragma unroll
+            for (int k = 0; k <= KM; ++k) copy(k, wp[d], d, make_uint2(0u, 0u));
+            stage_rows(wp[d], smem + d * S::BUF);
+            advance();
+        }
+        __builtin_amdgcn_s_barrier();  // (A)
+        asm volatile("" ::: "memory");
+#pragma unroll
+        for (int d = 0; d < D - 1; ++d) {
+#pragma unroll
+            for (int k = KM + 1; k < S::COPIES; ++k) copy(k, wp[d], d, o[d]);
+        }
+        uint2 onx = om_at(ic, cur_w());  // entry of element D-1
+        if constexpr (VEC)
+            wait_vmcnt_le<(D - 2) * S::CA>();  // element 0 landed
+        else
+            __builtin_amdgcn_s_waitcnt(0);
+        __builtin_amdgcn_s_barrier();  // (B)
+        asm volatile("" ::: "memory");
+
+        // step e: copies of element e+D-1 into the buffer of element e-1; the
+        // overflow entry of the next element loads across the next barrier
+        auto cstep = [&](int64_t e, int u) {
+            if (e + 1 < steps) {
+                if constexpr (VEC)
+                    wait_window_landed<D, S::CA, S::COPIES>((int)(e < D ? e : D));
+                else
+                    __builtin_amdgcn_s_waitcnt(0);
+            }
+            // a bare barrier: __syncthreads() would also wait for the later
+            // elements' copies still in flight
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");
+            const int b = (u + D - 1) % D;
+            const int w = cur_w();
+#pragma unroll
+            for (int k = 0; k < S::COPIES; ++k) copy(k, w, b, onx);
+            stage_rows(w, smem + b * S::BUF);
+            advance();
+            onx = om_at(ic, cur_w());
+        };
+        constexpr int U = D;  // unroll: the buffer index repeats
+        int64_t e = 0;
+        for (; e + U <= steps; e += U) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) cstep(e + u, u);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (e + u < steps) cstep(e + u, u);
+        __builtin_amdgcn_s_waitcnt(0);  // no copy may land after the workgroup ends
+        return;
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // the epilogue table's LDS stores are done
+    __builtin_amdgcn_s_barrier();   // (A)
+    asm volatile("" ::: "memory");
+
+    // ---- compute waves
 
     // this lane's B rows (token (lane & 15) of each subtile) and 32-column
     // slice of the window: pieces 2h and 2h+1, h = lane / 16
@@ -357,15 +540,15 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
     // this lane's index word: block-row (lane%16)/4, lane group lane/16
     const int iword = ((lane & 15) >> 2) * 4 + (lane >> 4);
 
-    // Operands of one window in registers: B (token rows), main and overflow
-    // A operands with their index words. Two sets alternate (steps w and w+1).
+    // Operands of one element in registers: B (token rows), main and overflow
+    // A operands with their index words. Two sets alternate (steps e, e+1).
     struct Ops {
         i32x8 bv[ST];
         i32x4 av[CT], ao[CT];
         int ix[CT], io[CT];
     };
     Ops ops[2];
-    // main operands (B rows, main A and index words) of one window
+    // main operands (B rows, main A and index words) of one element
     auto read_main = [&](Ops &r, const int8_t *b) {
 #pragma unroll
         for (int s = 0; s < ST; ++s) {
@@ -380,134 +563,92 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
             r.ix[c] = *reinterpret_cast<const int *>(op + 1024 + iword * 4);
         }
     };
-    // overflow operand of tile c of one window (read only if the tile has one)
+    // overflow operand of tile c of one element (read only if the tile has one)
     auto read_ovf = [&](Ops &r, const int8_t *b, int c) {
         const int8_t *oo = b + S::XB + S::AB + (wn * CT + c) * kOpBytes;
         r.ao[c] = *reinterpret_cast<const i32x4 *>(oo + lane * 16);
         r.io[c] = *reinterpret_cast<const int *>(oo + 1024 + iword * 4);
     };
-    auto read_ops = [&](Ops &r, const int8_t *b, uint32_t mask) {
-        read_main(r, b);
-#pragma unroll
-        for (int c = 0; c < CT; ++c)
-            if ((mask >> (wn * CT + c)) & 1u) read_ovf(r, b, c);  // (ao, io used only under the same condition)
-    };
-    // overflow entry (mask, first index) of window w for this workgroup's
-    // tiles, from the table built at packing; the address is uniform, so it is
-    // a scalar load, counted apart from the copies
-    typedef const __attribute__((address_space(4))) uint64_t *const_u64_ptr;
-    const const_u64_ptr omt = (const_u64_ptr)(a.om) + cg;
-    auto om_at = [&](int w) {
-        const uint64_t v = omt[(size_t)w * a.n_cgroups];
-        return make_uint2((uint32_t)v, (uint32_t)(v >> 32));
-    };
+    auto read_mask = [&](int b) { return (uint32_t)__builtin_amdgcn_readfirstlane((int)omask[b * S::NW]); };
 
-    // Software pipeline over windows, one barrier per window. In step w
-    //  * the copy waves wait until window w+1 has landed (at most D-3 later
-    //    windows' copies outstanding), pass the barrier, and start the copies
-    //    of window w+D-1 into the buffer of window w-1;
-    //  * the compute waves pass the barrier, read window w+1's operands into
-    //    one register set while the matrix instructions of window w run from
-    //    the other.
-    // The barrier after the copy waves' wait makes window w+1 visible, and
-    // means every compute wave has finished reading window w-1's buffer
-    // (those reads were consumed by the previous step's matrix instructions).
-    static_assert(D >= 3, "the pipeline reads one window ahead of the one it multiplies");
-    static_assert((D - 2) * S::COPIES < 64, "outstanding copies must fit the 6-bit vector-memory counter");
-    constexpr int U = D % 2 ? 2 * D : D;  // unroll: buffer index and register set both repeat
-
-    // Prologue. The copy waves start the weight scales and biases, and the
-    // token rows and main operands of windows 0..D-2, while their overflow
-    // entries load; the compute waves fill the epilogue table. A bare barrier
-    // (A) publishes the table, then the copy waves add the overflow operands
-    // of windows 0..D-2 and wait for window 0; a second barrier (B) publishes
-    // it.
-    if (copier) {
-        if (pw == 0 && KIND != SL_EPI_ACC_I32) {
-            static_assert(S::NT * 16 * 4 <= 1024, "scales of one workgroup fit one copy");
+    // This wave's weight scales and biases of an item (CT tiles x 16 channels
+    // each) go into its own LDS area with one copy per vector at the item's
+    // first window; the epilogue reads them after waiting for its own copies.
+    float *vec = reinterpret_cast<float *>(smem + S::LDS + (KIND == SL_EPI_I8_GELU ? kGeluLds : 0) + wave * kVecLds);
+    static_assert(CT * kTileN * 4 <= kVecLds / 2, "a wave's scales fit one copy");
+    auto fetch_vec = [&](const ItemIter &it) {
+        if constexpr (KIND != SL_EPI_ACC_I32) {
             const __amdgpu_buffer_rsrc_t sr =
                 __builtin_amdgcn_make_buffer_rsrc((void *)a.w_scale, 0, a.n * 4, kRsrcWord3);
             const __amdgpu_buffer_rsrc_t br = __builtin_amdgcn_make_buffer_rsrc((void *)a.bias, 0, a.n * 4, kRsrcWord3);
-            const uint32_t vo = lane < S::NT * 4 ? (uint32_t)((tile0 * 16 + lane * 4) * 4) : kOob;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(sr, (lds_void *)(smem + S::LDS), 16, vo, 0, 0, 0);
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(br, (lds_void *)(smem + S::LDS + 1024), 16, vo, 0, 0, 0);
-        }
-#pragma unroll
-        for (int d = 0; d < D - 1; ++d) {
-#pragma unroll
-            for (int k = 0; k < S::CX + S::CA; ++k) copy(k, phys(d), smem + d * S::BUF, 0u, 0u);
-            stage_rows(phys(d), smem + d * S::BUF);
-        }
-        __builtin_amdgcn_s_barrier();  // (A)
-        asm volatile("" ::: "memory");
-    } else {
-        __builtin_amdgcn_s_waitcnt(0);  // the epilogue table's LDS stores are done
-        __builtin_amdgcn_s_barrier();   // (A)
-        asm volatile("" ::: "memory");
-    }
-    if (copier) {
-        auto cstep = [&](int w, int u) {
-            if (w + 1 < a.n_win) {
-                if constexpr (VEC)
-                    wait_window_landed<D, S::CA, S::COPIES>(w);
-                else
-                    __builtin_amdgcn_s_waitcnt(0);
+            // only the first CT*4 lanes copy (16 bytes each), so a copy fills
+            // CT*64 bytes of LDS
+            if (lane < CT * 4) {
+                const uint32_t off = (uint32_t)(((it.cg * S::NT + wn * CT) * kTileN + lane * 4) * 4);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(sr, (lds_void *)vec, 16, off, 0, 0, 0);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(br, (lds_void *)(vec + kVecLds / 8), 16, off, 0, 0, 0);
             }
-            // a bare barrier: __syncthreads() would also wait for the later
-            // windows' copies still in flight
-            __builtin_amdgcn_s_barrier();
-            asm volatile("" ::: "memory");
-            // past the end: a harmless repeat (of the last window in this
-            // workgroup's order) keeps the copy count fixed
-            const int wcp = phys(w + D - 1);
-            const uint2 o = om_at(wcp);
-            int8_t *nb = smem + ((u + D - 1) % D) * S::BUF;
-#pragma unroll
-            for (int k = 0; k < S::COPIES; ++k) copy(k, wcp, nb, o.x, o.y);
-            stage_rows(wcp, nb);
-        };
-#pragma unroll
-        for (int d = 0; d < D - 1; ++d) {
-            const uint2 od = om_at(phys(d));
-#pragma unroll
-            for (int k = S::CX + S::CA; k < S::COPIES; ++k) copy(k, phys(d), smem + d * S::BUF, od.x, od.y);
         }
-        if constexpr (VEC)
-            wait_vmcnt_le<(D - 2) * S::CA>();  // window 0 (and the scales) landed
-        else
-            __builtin_amdgcn_s_waitcnt(0);
-        __builtin_amdgcn_s_barrier();  // (B)
-        asm volatile("" ::: "memory");
-        int w = 0;
-        for (; w + U <= a.n_win; w += U) {
-#pragma unroll
-            for (int u = 0; u < U; ++u) cstep(w + u, u);
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u)
-            if (w + u < a.n_win) cstep(w + u, u);
-        __builtin_amdgcn_s_waitcnt(0);  // no copy may land after the workgroup ends
-        return;
-    }
+    };
 
-    // compute waves
-    // mask_w: overflow mask of window w (its operands are in ops[u & 1]);
-    // mask_n: of window w+1
-    uint32_t mask_w, mask_n;
-    auto step = [&](int w, int u) {
-        Ops &cur = ops[u & 1];
-        Ops &nxt = ops[(u + 1) & 1];
+    i32x4 acc[CT][ST];
+    auto clear_acc = [&]() {
+#pragma unroll
+        for (int c = 0; c < CT; ++c)
+#pragma unroll
+            for (int s = 0; s < ST; ++s) acc[c][s] = i32x4{0, 0, 0, 0};
+    };
+    // accumulator layout: lane l holds rows 4*(l/16)+r (channels of one
+    // block-row), column l%16 (token), r = 0..3
+    auto epilogue = [&](const ItemIter &it) {
+        __builtin_amdgcn_s_waitcnt(0);  // this wave's scale and bias copies
+        const int64_t m0 = (int64_t)it.mt * S::TM;
+#pragma unroll
+        for (int c = 0; c < CT; ++c) {
+            const int32_t t = it.cg * S::NT + wn * CT + c;
+            if (t >= a.n_tiles) break;
+            const int32_t ch0 = t * kTileN + 4 * (lane >> 4);
+            if (ch0 >= a.n) continue;  // block-rows past n_out in the last tile
+            float s[4] = {0, 0, 0, 0}, bb4[4] = {0, 0, 0, 0};
+            if constexpr (KIND != SL_EPI_ACC_I32) {
+                const int lc = c * kTileN + 4 * (lane >> 4);  // channel within the wave's tiles
+                const float4 sw = *reinterpret_cast<const float4 *>(vec + lc);
+                const float4 bb = *reinterpret_cast<const float4 *>(vec + kVecLds / 8 + lc);
+                s[0] = a.sx * sw.x;
+                s[1] = a.sx * sw.y;
+                s[2] = a.sx * sw.z;
+                s[3] = a.sx * sw.w;
+                bb4[0] = bb.x;
+                bb4[1] = bb.y;
+                bb4[2] = bb.z;
+                bb4[3] = bb.w;
+            }
+#pragma unroll
+            for (int st = 0; st < ST; ++st)
+                epilogue_store<KIND>(a, acc[c][st], m0 + wm * ST * 16 + st * 16 + (lane & 15), ch0, s, bb4, tab, hinv,
+                                     eoff, cmax);
+        }
+    };
+
+    // sl: ring buffer of element e; mask_w: overflow mask of element e (its
+    // operands are in register set PR)
+    int sl = 0;
+    int64_t e = 0;
+    uint32_t mask_w;
+    auto step = [&](auto pr) {
+        constexpr int PR = decltype(pr)::value;
+        Ops &cur = ops[PR];
+        Ops &nxt = ops[PR ^ 1];
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
-        const uint32_t mask_n2 = om_at(phys(w + 2)).x;
-        const int8_t *nb = smem + ((u + 1) % D) * S::BUF;
-        // Main part: window w+1's main operand reads and window w's main
+        const int sl1 = sl + 1 == D ? 0 : sl + 1;
+        const int8_t *nb = smem + sl1 * S::BUF;
+        // Main part: element e+1's main operand reads and element e's main
         // matrix instructions, one after the other, so that a read waiting
         // for room in the LDS queue does not leave the matrix core idle.
-        // (The last step reads nothing: the barrier has already passed, so
-        // reading a stale buffer is harmless and keeps the code branch-free.)
-        // Main products of tiles past n_tiles land in accumulators that are
-        // never stored, so they need no branch either.
+        // (The last step reads a stale buffer: harmless, and branch-free.)
+        // Main products of tiles past the item's last tile land in
+        // accumulators that are never stored, so they need no branch either.
         read_main(nxt, nb);
 #pragma unroll
         for (int c = 0; c < CT; ++c)
@@ -520,11 +661,15 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one matrix instruction
         }
         __builtin_amdgcn_sched_group_barrier(0x100, 2 * ST + 2 * CT, 0);  // the remaining reads
+        // element e+1's overflow mask, read once the main matrix instructions
+        // are queued (its latency hides behind them)
+        __builtin_amdgcn_sched_barrier(0);
+        const uint32_t mask_n = read_mask(sl1);
         // overflow part, per tile
 #pragma unroll
         for (int c = 0; c < CT; ++c) {
             const int jw = wn * CT + c;
-            if (w + 1 < a.n_win && ((mask_n >> jw) & 1u)) read_ovf(nxt, nb, c);
+            if (e + 1 < steps && ((mask_n >> jw) & 1u)) read_ovf(nxt, nb, c);
             if ((mask_w >> jw) & 1u) {
 #pragma unroll
                 for (int s = 0; s < ST; ++s)
@@ -533,50 +678,41 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
             }
         }
         mask_w = mask_n;
-        mask_n = mask_n2;
+        sl = sl1;
+        ++e;
     };
-    __builtin_amdgcn_s_barrier();  // (B): window 0 has landed
-    asm volatile("" ::: "memory");
-    mask_w = om_at(phys(0)).x;
-    mask_n = om_at(phys(1)).x;
-    read_ops(ops[0], smem, mask_w);
-    {
-        int w = 0;
-        for (; w + U <= a.n_win; w += U) {
-#pragma unroll
-            for (int u = 0; u < U; ++u) step(w + u, u);
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u)
-            if (w + u < a.n_win) step(w + u, u);
-    }
+    using P0 = std::integral_constant<int, 0>;
+    using P1 = std::integral_constant<int, 1>;
 
-    // accumulator layout: lane l holds rows 4*(l/16)+r (channels of one
-    // block-row), column l%16 (token), r = 0..3
+    ItemIter it = first;
+    clear_acc();
+    fetch_vec(it);
+    __builtin_amdgcn_s_barrier();  // (B): element 0 has landed
+    asm volatile("" ::: "memory");
+    mask_w = read_mask(0);
+    read_main(ops[0], smem);
 #pragma unroll
-    for (int c = 0; c < CT; ++c) {
-        const int32_t t = tile0 + wn * CT + c;
-        if (t >= a.n_tiles) break;
-        const int32_t ch0 = t * kTileN + 4 * (lane >> 4);
-        if (ch0 >= a.n) continue;  // block-rows past n_out in the last tile
-        float s[4] = {0, 0, 0, 0}, bb4[4] = {0, 0, 0, 0};
-        if constexpr (KIND != SL_EPI_ACC_I32) {
-            const int lc = (wn * CT + c) * kTileN + 4 * (lane >> 4);  // channel within the workgroup
-            const float4 sw = *reinterpret_cast<const float4 *>(vec_sw + lc);
-            const float4 bb = *reinterpret_cast<const float4 *>(vec_b + lc);
-            s[0] = a.sx * sw.x;
-            s[1] = a.sx * sw.y;
-            s[2] = a.sx * sw.z;
-            s[3] = a.sx * sw.w;
-            bb4[0] = bb.x;
-            bb4[1] = bb.y;
-            bb4[2] = bb.z;
-            bb4[3] = bb.w;
+    for (int c = 0; c < CT; ++c)
+        if ((mask_w >> (wn * CT + c)) & 1u) read_ovf(ops[0], smem, c);
+    // Each item starts with its first element's operands in register set 0;
+    // after an odd number of windows they are moved there from set 1.
+    for (int k = 0; k < n_my; ++k) {
+        int w = 0;
+        for (; w + 2 <= a.n_win; w += 2) {
+            step(P0{});
+            step(P1{});
         }
-#pragma unroll
-        for (int st = 0; st < ST; ++st)
-            epilogue_store<KIND>(a, acc[c][st], m0 + wm * ST * 16 + st * 16 + (lane & 15), ch0, s, bb4, tab, hinv,
-                                 eoff, cmax);
+        if (w < a.n_win) {
+            step(P0{});
+            ops[0] = ops[1];
+        }
+        epilogue(it);
+        if (k + 1 < n_my) {
+            clear_acc();
+            it.next();
+            asm volatile("" ::: "memory");  // the epilogue's reads of the scales come first
+            fetch_vec(it);
+        }
     }
 }
 
@@ -747,7 +883,7 @@ void release_image(sl_packed_weight *w)
 }
 
 template <int KIND, int ST, int CT, int WM, int WN, int D, bool VEC>
-static sl_status launch_cfg(const LinearArgs &a, const GeluArg *ep, int64_t nwg, hipStream_t stream)
+static sl_status launch_cfg(const LinearArgs &a, const GeluArg *ep, hipStream_t stream)
 {
     using S = Shape<ST, CT, WM, WN, D>;
     const void *fn;
@@ -760,8 +896,25 @@ static sl_status launch_cfg(const LinearArgs &a, const GeluArg *ep, int64_t nwg,
         HIP_TRY(hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, kLdsMax));
         attr_done = true;
     }
-    const size_t lds = (size_t)S::LDS + kVecLds + (KIND == SL_EPI_I8_GELU ? kGeluCells * sizeof(GeluCell) : 0);
-    static_assert(S::LDS + kVecLds + kGeluCells * sizeof(GeluCell) <= kLdsMax, "workgroup shape exceeds LDS");
+    const size_t lds = (size_t)S::LDS + S::NW * kVecLds + kMaskLds + (KIND == SL_EPI_I8_GELU ? kGeluLds : 0);
+    static_assert(S::LDS + S::NW * kVecLds + kMaskLds + kGeluLds <= kLdsMax, "workgroup shape exceeds LDS");
+    static_assert(D * S::NW * 4 <= kMaskLds, "one overflow mask per ring buffer and copy wave");
+    // persistent grid: as many workgroups as fit on the device at once, each
+    // taking every G-th work item
+    static int resident[kMaxDevices] = {};  // per kernel instance and device; benign race as above
+    int dev = 0;
+    HIP_TRY(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxDevices) {
+        set_error("device index beyond the supported range");
+        return SL_ERR_UNSUPPORTED;
+    }
+    if (!resident[dev]) {
+        int per_cu = 0, n_cu = 0;
+        HIP_TRY(hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev));
+        HIP_TRY(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, S::NTHG, lds));
+        resident[dev] = std::max(1, per_cu) * std::max(1, n_cu);
+    }
+    const int64_t nwg = std::min<int64_t>(a.n_items, resident[dev]);
     if constexpr (KIND == SL_EPI_I8_GELU)
         hipLaunchKernelGGL((sparse_linear_gelu_kernel<ST, CT, WM, WN, D, VEC>), dim3((uint32_t)nwg), dim3(S::NTHG),
                            lds, stream, a, *ep);
@@ -773,25 +926,24 @@ static sl_status launch_cfg(const LinearArgs &a, const GeluArg *ep, int64_t nwg,
 }
 
 template <int KIND, bool VEC>
-static sl_status launch_kind(const LinearArgs &a, const GeluArg *ep, TileCfg c, int64_t nwg, hipStream_t stream)
+static sl_status launch_kind(const LinearArgs &a, const GeluArg *ep, TileCfg c, hipStream_t stream)
 {
 #define SL_CFG(A_, B_, C_, D_, E_)                                         \
     if (c.st == A_ && c.ct == B_ && c.wm == C_ && c.wn == D_ && c.d == E_) \
-        return launch_cfg<KIND, A_, B_, C_, D_, E_, VEC>(a, ep, nwg, stream);
+        return launch_cfg<KIND, A_, B_, C_, D_, E_, VEC>(a, ep, stream);
     SL_CFG(4, 3, 2, 2, 3)
     SL_CFG(4, 3, 2, 2, 4)
     SL_CFG(2, 3, 2, 2, 3)
     SL_CFG(2, 3, 2, 2, 4)
     SL_CFG(1, 3, 2, 2, 6)
 #undef SL_CFG
-    return launch_cfg<KIND, 1, 1, 2, 2, 8, VEC>(a, ep, nwg, stream);
+    return launch_cfg<KIND, 1, 1, 2, 2, 8, VEC>(a, ep, stream);
 }
 
 template <int KIND>
-static sl_status launch_vec(const LinearArgs &a, const GeluArg *ep, TileCfg c, int64_t nwg, hipStream_t stream,
-                            bool vec)
+static sl_status launch_vec(const LinearArgs &a, const GeluArg *ep, TileCfg c, hipStream_t stream, bool vec)
 {
-    return vec ? launch_kind<KIND, true>(a, ep, c, nwg, stream) : launch_kind<KIND, false>(a, ep, c, nwg, stream);
+    return vec ? launch_kind<KIND, true>(a, ep, c, stream) : launch_kind<KIND, false>(a, ep, c, stream);
 }
 
 // Pick the workgroup shape: among shapes that give every CU a workgroup,
@@ -891,19 +1043,19 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int64_t m, f
             return SL_ERR_UNSUPPORTED;
         }
         const int64_t mt = (a.m + cfg.tm() - 1) / cfg.tm();
-        const int64_t nwg = mt * a.n_cgroups;
-        if (nwg > 0x7fffffff) {
-            set_error("too many workgroups for one launch");
+        a.n_items = mt * a.n_cgroups;
+        if (a.n_items > 0x7fffffff) {
+            set_error("too many work items for one launch");
             return SL_ERR_UNSUPPORTED;
         }
         sl_status st;
         switch (run_kind) {
-        case SL_EPI_ACC_I32: st = launch_vec<SL_EPI_ACC_I32>(a, nullptr, cfg, nwg, s, vec); break;
-        case SL_EPI_F32: st = launch_vec<SL_EPI_F32>(a, nullptr, cfg, nwg, s, vec); break;
-        case SL_EPI_F32_GELU: st = launch_vec<SL_EPI_F32_GELU>(a, nullptr, cfg, nwg, s, vec); break;
-        case SL_EPI_I8: st = launch_vec<SL_EPI_I8>(a, nullptr, cfg, nwg, s, vec); break;
-        case SL_EPI_I8_GELU: st = launch_vec<SL_EPI_I8_GELU>(a, &ga, cfg, nwg, s, vec); break;
-        default: st = launch_vec<kEpiI8GeluErf>(a, nullptr, cfg, nwg, s, vec); break;
+        case SL_EPI_ACC_I32: st = launch_vec<SL_EPI_ACC_I32>(a, nullptr, cfg, s, vec); break;
+        case SL_EPI_F32: st = launch_vec<SL_EPI_F32>(a, nullptr, cfg, s, vec); break;
+        case SL_EPI_F32_GELU: st = launch_vec<SL_EPI_F32_GELU>(a, nullptr, cfg, s, vec); break;
+        case SL_EPI_I8: st = launch_vec<SL_EPI_I8>(a, nullptr, cfg, s, vec); break;
+        case SL_EPI_I8_GELU: st = launch_vec<SL_EPI_I8_GELU>(a, &ga, cfg, s, vec); break;
+        default: st = launch_vec<kEpiI8GeluErf>(a, nullptr, cfg, s, vec); break;
         }
         if (st != SL_OK) return st;
     }
