@@ -39,56 +39,10 @@
 #include <string>
 #include <type_traits>
 
-#include "sl_internal.h"
+#include "sl_device.h"
 
 namespace sl {
 
-typedef int i32x4 __attribute__((ext_vector_type(4)));
-typedef int i32x8 __attribute__((ext_vector_type(8)));
-
-constexpr int kXcds = 8;  // accelerator complex dies, each with its own L2
-constexpr int kMaxDevices = 64;
-// Buffer-load offset past any buffer this library reads (all < 2 GiB): such
-// a lane reads zeros. Buffer word 3 for raw byte loads on gfx9.
-constexpr uint32_t kOob = 0x80000000u;
-constexpr int32_t kRsrcWord3 = 0x00020000;
-constexpr int64_t kMaxBufferBytes = 0x7ff00000;  // per launch: token chunk bytes and weight image
-// per workgroup, ahead of the windows: its output channels' weight scales
-// and biases (one 1 KiB copy each, read by the epilogue from LDS)
-constexpr int kVecLds = 512;  // a compute wave's weight scales and biases
-constexpr int kGeluLds = (kGeluCells * (int)sizeof(GeluCell) + 15) / 16 * 16;
-constexpr int kMaskLds = 256;  // the ring buffers' overflow masks
-constexpr size_t kLdsMax = 160 * 1024; // LDS per workgroup on gfx950
-
-#define HIP_TRY(expr)                                                                     \
-    do {                                                                                  \
-        hipError_t e_ = (expr);                                                           \
-        if (e_ != hipSuccess) {                                                           \
-            set_error(std::string(#expr) + ": " + hipGetErrorString(e_));                 \
-            return SL_ERR_HIP;                                                            \
-        }                                                                                 \
-    } while (0)
-
-struct LinearArgs {
-    const int8_t *x;
-    void *y;
-    int64_t m;
-    int32_t n;
-    int32_t k;
-    const int8_t *main;
-    const int8_t *ovf;
-    uint32_t main_bytes;  // image sizes: the range of the buffer loads
-    uint32_t ovf_bytes;
-    const uint32_t *om;  // overflow table of this launch's tile-group size, [n_win][n_cgroups][2]
-    const float *w_scale;
-    const float *bias;
-    float sx;
-    float inv_so;
-    int32_t n_tiles;
-    int32_t n_win;
-    int32_t n_cgroups;  // channel groups of NT tiles
-    int64_t n_items;    // work items: token tiles x channel groups
-};
 
 // Workgroup shape: WM x WN waves; a wave owns ST 16-token subtiles x CT
 // 16-channel tiles; D windows are in flight (D LDS buffers). One window's
@@ -120,153 +74,6 @@ struct Shape {
 // 8 consecutive rows in 8), so the reads are free of bank conflicts.
 __device__ __forceinline__ int xsw(int r) { return (r ^ (r >> 3)) & 7; }
 
-// internal kind: GELU + requantisation evaluated with erf (no usable table)
-constexpr int kEpiI8GeluErf = 5;
-
-// The GELU + requantisation step table, passed by value to the kernel of
-// SL_EPI_I8_GELU.
-struct GeluArg {
-    float hinv, off;
-    int32_t nc, pad;
-    GeluCell cell[kGeluCells];
-};
-
-// Workgroups are dispatched round-robin over the XCDs. Renumber them so that
-// each XCD runs a contiguous range of work items; adjacent work items share a
-// token tile, so that tile's rows are fetched into one L2.
-__device__ __forceinline__ int64_t xcd_work_index(int64_t bid, int64_t nwg)
-{
-    const int64_t q = nwg / kXcds, r = nwg % kXcds;
-    const int64_t x = bid % kXcds, j = bid / kXcds;
-    return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + j;
-}
-
-// GELU, erf form, in the same fp32 operation order as the definition.
-__device__ __forceinline__ float gelu_erf(float y)
-{
-#pragma clang fp contract(off)
-    const float t = y * 0.70710678118654752f;
-    const float e = erff(t);
-    const float h = 0.5f * y;
-    const float one_e = 1.0f + e;
-    return h * one_e;
-}
-
-__device__ __forceinline__ int32_t requant_i8(float g, float inv_so)
-{
-#pragma clang fp contract(off)
-    const float v = g * inv_so;
-    float r = __builtin_rintf(v);
-    r = fminf(fmaxf(r, -127.0f), 127.0f);
-    return (int32_t)r;
-}
-
-template <int KIND>
-__device__ __forceinline__ void epilogue_store(const LinearArgs &a, const i32x4 acc, int64_t tok, int32_t ch0,
-                                               const float s[4], const float b[4], const GeluCell *tab,
-                                               float hinv, float off, float cmax)
-{
-#pragma clang fp contract(off)
-    if (tok >= a.m) return;
-    const int64_t off64 = tok * a.n + ch0;
-    if constexpr (KIND == SL_EPI_ACC_I32) {
-        *reinterpret_cast<i32x4 *>(static_cast<int32_t *>(a.y) + off64) = acc;
-    } else if constexpr (KIND == SL_EPI_I8_GELU) {
-        uint32_t packed = 0;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            float y = (float)acc[r] * s[r];
-            y = y + b[r];
-            const float c = __builtin_amdgcn_fmed3f(__builtin_fmaf(y, hinv, off), 0.0f, cmax);
-            const GeluCell e = tab[(int)c];
-            const int q = y >= e.thr ? e.q_hi : e.q_lo;
-            packed |= ((uint32_t)q & 0xffu) << (8 * r);
-        }
-        *reinterpret_cast<uint32_t *>(static_cast<int8_t *>(a.y) + off64) = packed;
-    } else {
-        float g[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            float y = (float)acc[r] * s[r];
-            y = y + b[r];
-            g[r] = (KIND == SL_EPI_F32_GELU || KIND == kEpiI8GeluErf) ? gelu_erf(y) : y;
-        }
-        if constexpr (KIND == SL_EPI_F32 || KIND == SL_EPI_F32_GELU) {
-            *reinterpret_cast<float4 *>(static_cast<float *>(a.y) + off64) = make_float4(g[0], g[1], g[2], g[3]);
-        } else {
-            uint32_t packed = 0;
-#pragma unroll
-            for (int r = 0; r < 4; ++r) packed |= ((uint32_t)requant_i8(g[r], a.inv_so) & 0xffu) << (8 * r);
-            *reinterpret_cast<uint32_t *>(static_cast<int8_t *>(a.y) + off64) = packed;
-        }
-    }
-}
-
-typedef __attribute__((address_space(3))) void lds_void;
-
-// s_waitcnt with only the vector-memory count constrained (<= N outstanding)
-template <int N>
-__device__ __forceinline__ void wait_vmcnt_le()
-{
-    static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
-    // gfx9 encoding: vmcnt [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8]
-    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-
-// Copy waves, start of step w: wait until element w+1 has landed. The copies
-// issued after element w+1's last copy may stay outstanding: in the prologue
-// order (token rows, main operands and overflow mask of elements 0..D-2, then
-// their overflow operands) that is the overflow copies of elements w+2..D-2
-// plus the elements copied in steps 0..w-1, later the D-3 elements copied
-// after it.
-template <int D, int CA, int COPIES, int I = 0>
-__device__ __forceinline__ void wait_window_landed(int w)
-{
-    if constexpr (I < D - 3) {
-        if (w == I) {
-            wait_vmcnt_le<(D - 3 - I) * CA + I * COPIES>();
-            return;
-        }
-        wait_window_landed<D, CA, COPIES, I + 1>(w);
-    } else {
-        wait_vmcnt_le<(D - 3) * COPIES>();
-    }
-}
-
-// The work items of one workgroup: slot, slot + G, slot + 2G, ... as token
-// tile mt, channel group cg and window rotation rot (items walk the windows
-// from different starting points; integer accumulation does not depend on
-// the order, and the workgroups that share an input or weight line then
-// fetch it at different times). next() advances by G without dividing.
-struct ItemIter {
-    int32_t mt, cg, rot;
-    int32_t dmt, dcg, drot;
-    int32_t n_cgroups, n_win;
-    __device__ static ItemIter start(int32_t slot, int32_t g, int32_t n_cgroups, int32_t n_win)
-    {
-        ItemIter it;
-        it.mt = slot / n_cgroups;
-        it.cg = slot - it.mt * n_cgroups;
-        it.rot = (int32_t)(((int64_t)slot * 7) % n_win);
-        it.dmt = g / n_cgroups;
-        it.dcg = g - it.dmt * n_cgroups;
-        it.drot = (int32_t)(((int64_t)g * 7) % n_win);
-        it.n_cgroups = n_cgroups;
-        it.n_win = n_win;
-        return it;
-    }
-    __device__ void next()
-    {
-        mt += dmt;
-        cg += dcg;
-        if (cg >= n_cgroups) {
-            cg -= n_cgroups;
-            ++mt;
-        }
-        rot += drot;
-        if (rot >= n_win) rot -= n_win;
-    }
-};
 
 // VEC: X rows are 16-byte aligned and k % 16 == 0, so token rows are copied
 // to LDS with 16-byte direct loads; otherwise they are staged byte by byte.
@@ -327,15 +134,16 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
     // Software pipeline over the element stream, one barrier per element. In
     // step e
     //  * the copy waves wait until element e+1 has landed, pass the barrier,
-    //    and start the copies of element e+D-1 into the buffer of element e-1;
+    //    and start the copies of element e+D into the buffer of element e;
     //  * the compute waves pass the barrier, read element e+1's operands into
     //    one register set while the matrix instructions of element e run from
-    //    the other, and after an item's last window run its epilogue.
+    //    the other, wait until those reads are done, and after an item's last
+    //    window run its epilogue.
     // The barrier after the copy waves' wait makes element e+1 visible, and
-    // means every compute wave has finished reading element e-1's buffer
-    // (those reads were consumed by the previous step's matrix instructions).
+    // means every compute wave has finished reading element e's buffer (read
+    // into registers in the previous step), so D-1 elements are in flight.
     static_assert(D >= 3, "the pipeline reads one element ahead of the one it multiplies");
-    static_assert((D - 2) * S::COPIES < 64, "outstanding copies must fit the 6-bit vector-memory counter");
+    static_assert((D - 1) * S::COPIES < 64, "outstanding copies must fit the 6-bit vector-memory counter");
 
     if (copier) {
         // Copies go through buffer loads (a lane's offset plus a scalar window
@@ -443,17 +251,17 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
             }
         };
 
-        // Prologue: the overflow entries of elements 0..D-2 start loading, the
+        // Prologue: the overflow entries of elements 0..D-1 start loading, the
         // token rows, main operands and overflow masks of those elements are
         // copied, a bare barrier (A) publishes the epilogue table the compute
         // waves filled, then the overflow operands follow; once element 0 has
         // landed a second barrier (B) publishes it.
-        uint2 o[D - 1];
+        uint2 o[D];
         {
             const ItemIter ic0 = ic;
             const int kc0 = kc, wc0 = wc;
 #pragma unroll
-            for (int d = 0; d < D - 1; ++d) {
+            for (int d = 0; d < D; ++d) {
                 o[d] = om_at(ic, cur_w());
                 if (++wc == a.n_win) {
                     wc = 0;
@@ -464,9 +272,9 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
             kc = kc0;
             wc = wc0;
         }
-        int wp[D - 1];
+        int wp[D];
 #pragma unroll
-        for (int d = 0; d < D - 1; ++d) {
+        for (int d = 0; d < D; ++d) {
             wp[d] = cur_w();
 #pragma unroll
             for (int k = 0; k <= KM; ++k) copy(k, wp[d], d, make_uint2(0u, 0u));
@@ -476,19 +284,19 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
         __builtin_amdgcn_s_barrier();  // (A)
         asm volatile("" ::: "memory");
 #pragma unroll
-        for (int d = 0; d < D - 1; ++d) {
+        for (int d = 0; d < D; ++d) {
 #pragma unroll
             for (int k = KM + 1; k < S::COPIES; ++k) copy(k, wp[d], d, o[d]);
         }
-        uint2 onx = om_at(ic, cur_w());  // entry of element D-1
+        uint2 onx = om_at(ic, cur_w());  // entry of element D
         if constexpr (VEC)
-            wait_vmcnt_le<(D - 2) * S::CA>();  // element 0 landed
+            wait_vmcnt_le<(D - 1) * S::CA>();  // element 0 landed
         else
             __builtin_amdgcn_s_waitcnt(0);
         __builtin_amdgcn_s_barrier();  // (B)
         asm volatile("" ::: "memory");
 
-        // step e: copies of element e+D-1 into the buffer of element e-1; the
+        // step e: copies of element e+D into the buffer of element e; the
         // overflow entry of the next element loads across the next barrier
         auto cstep = [&](int64_t e, int u) {
             if (e + 1 < steps) {
@@ -501,7 +309,7 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
             // elements' copies still in flight
             __builtin_amdgcn_s_barrier();
             asm volatile("" ::: "memory");
-            const int b = (u + D - 1) % D;
+            const int b = u;
             const int w = cur_w();
 #pragma unroll
             for (int k = 0; k < S::COPIES; ++k) copy(k, w, b, onx);
@@ -677,6 +485,9 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
                         __builtin_amdgcn_smfmac_i32_16x16x128_i8(cur.ao[c], cur.bv[s], acc[c][s], cur.io[c], 0, 0);
             }
         }
+        // element e+1's buffer is refilled after the next barrier: its
+        // reads must be done by then
+        wait_lgkm0();
         mask_w = mask_n;
         sl = sl1;
         ++e;
@@ -694,6 +505,7 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
 #pragma unroll
     for (int c = 0; c < CT; ++c)
         if ((mask_w >> (wn * CT + c)) & 1u) read_ovf(ops[0], smem, c);
+    wait_lgkm0();  // element 0's buffer is refilled after the next barrier
     // Each item starts with its first element's operands in register set 0;
     // after an odd number of windows they are moved there from set 1.
     for (int k = 0; k < n_my; ++k) {
@@ -806,6 +618,8 @@ sl_status upload_image(sl_packed_weight *w)
     std::vector<int> nts;
     for (const TileCfg &c : kCfgs)
         if (std::find(nts.begin(), nts.end(), c.nt()) == nts.end()) nts.push_back(c.nt());
+    for (const DirectCfg &c : kDirectCfgs)
+        if (std::find(nts.begin(), nts.end(), c.nt) == nts.end()) nts.push_back(c.nt);
     if ((int)nts.size() > kMaxOmTables) {
         set_error("internal: too many tile-group sizes");
         return SL_ERR_UNSUPPORTED;
@@ -882,6 +696,26 @@ void release_image(sl_packed_weight *w)
     w->on_device = false;
 }
 
+sl_status persistent_grid(const void *fn, int threads, size_t lds, int *cache, int *out)
+{
+    int dev = 0;
+    HIP_TRY(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxDevices) {
+        set_error("device index beyond the supported range");
+        return SL_ERR_UNSUPPORTED;
+    }
+    // a benign race: two threads may both fill the entry, with equal values
+    if (!cache[dev]) {
+        HIP_TRY(hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsMax));
+        int per_cu = 0, n_cu = 0;
+        HIP_TRY(hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev));
+        HIP_TRY(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, threads, lds));
+        cache[dev] = std::max(1, per_cu) * std::max(1, n_cu);
+    }
+    *out = cache[dev];
+    return SL_OK;
+}
+
 template <int KIND, int ST, int CT, int WM, int WN, int D, bool VEC>
 static sl_status launch_cfg(const LinearArgs &a, const GeluArg *ep, hipStream_t stream)
 {
@@ -891,30 +725,16 @@ static sl_status launch_cfg(const LinearArgs &a, const GeluArg *ep, hipStream_t 
         fn = reinterpret_cast<const void *>(&sparse_linear_gelu_kernel<ST, CT, WM, WN, D, VEC>);
     else
         fn = reinterpret_cast<const void *>(&sparse_linear_kernel<KIND, ST, CT, WM, WN, D, VEC>);
-    static bool attr_done = false;  // benign race: setting it twice is harmless
-    if (!attr_done) {
-        HIP_TRY(hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, kLdsMax));
-        attr_done = true;
-    }
     const size_t lds = (size_t)S::LDS + S::NW * kVecLds + kMaskLds + (KIND == SL_EPI_I8_GELU ? kGeluLds : 0);
     static_assert(S::LDS + S::NW * kVecLds + kMaskLds + kGeluLds <= kLdsMax, "workgroup shape exceeds LDS");
     static_assert(D * S::NW * 4 <= kMaskLds, "one overflow mask per ring buffer and copy wave");
     // persistent grid: as many workgroups as fit on the device at once, each
     // taking every G-th work item
-    static int resident[kMaxDevices] = {};  // per kernel instance and device; benign race as above
-    int dev = 0;
-    HIP_TRY(hipGetDevice(&dev));
-    if (dev < 0 || dev >= kMaxDevices) {
-        set_error("device index beyond the supported range");
-        return SL_ERR_UNSUPPORTED;
-    }
-    if (!resident[dev]) {
-        int per_cu = 0, n_cu = 0;
-        HIP_TRY(hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev));
-        HIP_TRY(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, S::NTHG, lds));
-        resident[dev] = std::max(1, per_cu) * std::max(1, n_cu);
-    }
-    const int64_t nwg = std::min<int64_t>(a.n_items, resident[dev]);
+    static int resident[kMaxDevices] = {};  // per kernel instance and device
+    int grid = 0;
+    const sl_status st = persistent_grid(fn, S::NTHG, lds, resident, &grid);
+    if (st != SL_OK) return st;
+    const int64_t nwg = std::min<int64_t>(a.n_items, grid);
     if constexpr (KIND == SL_EPI_I8_GELU)
         hipLaunchKernelGGL((sparse_linear_gelu_kernel<ST, CT, WM, WN, D, VEC>), dim3((uint32_t)nwg), dim3(S::NTHG),
                            lds, stream, a, *ep);
@@ -952,7 +772,7 @@ static sl_status launch_vec(const LinearArgs &a, const GeluArg *ep, TileCfg c, h
 // overrides (tuning; unknown shapes are ignored).
 static TileCfg choose_cfg(int64_t m, const sl_packed_weight *w)
 {
-    static const char *env = getenv("SL_TILE");
+    const char *env = getenv("SL_TILE");
     if (env) {
         TileCfg c;
         if (sscanf(env, "%d,%d,%d,%d,%d", &c.st, &c.ct, &c.wm, &c.wn, &c.d) == 5)
@@ -975,6 +795,40 @@ static TileCfg choose_cfg(int64_t m, const sl_packed_weight *w)
             most = &c;
         }
         if (nwg < 240) continue;
+        const double cost = xbytes * cgs + wbytes * mt;
+        if (!best || cost < best_cost) {
+            best = &c;
+            best_cost = cost;
+        }
+    }
+    return best ? *best : *most;
+}
+
+// Direct-kernel shape, by the same rule; SL_DTILE="st,nt,wm,d" overrides.
+static DirectCfg choose_direct_cfg(int64_t m, const sl_packed_weight *w)
+{
+    const char *env = getenv("SL_DTILE");
+    if (env) {
+        DirectCfg c;
+        if (sscanf(env, "%d,%d,%d,%d", &c.st, &c.nt, &c.wm, &c.d) == 4)
+            for (const DirectCfg &k : kDirectCfgs)
+                if (k.st == c.st && k.nt == c.nt && k.wm == c.wm && k.d == c.d) return k;
+    }
+    const int32_t n_tiles = w->tiles.n_tiles;
+    const double xbytes = (double)m * w->k_in;
+    const double wbytes = (double)w->tiles.main.size() + (double)w->tiles.ovf.size();
+    const DirectCfg *best = nullptr, *most = nullptr;
+    double best_cost = 0;
+    int64_t most_items = 0;
+    for (const DirectCfg &c : kDirectCfgs) {
+        const int64_t mt = (m + c.tm() - 1) / c.tm();
+        const int64_t cgs = (n_tiles + c.nt - 1) / c.nt;
+        const int64_t items = mt * cgs;
+        if (items > most_items) {
+            most_items = items;
+            most = &c;
+        }
+        if (items < 240) continue;
         const double cost = xbytes * cgs + wbytes * mt;
         if (!best || cost < best_cost) {
             best = &c;
@@ -1033,29 +887,48 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int64_t m, f
         a.y = static_cast<char *>(y) + t0 * w->n_out * out_bytes;
         a.m = std::min(chunk, m - t0);
         const bool vec = (w->k_in % 16 == 0) && ((reinterpret_cast<uintptr_t>(a.x) & 15) == 0);
-        const TileCfg cfg = choose_cfg(a.m, w);
-        a.n_cgroups = (ti.n_tiles + cfg.nt() - 1) / cfg.nt();
+        // row-major token rows go through the staged kernel; SL_PATH=direct
+        // selects the direct-operand kernel for aligned rows (tests, tuning)
+        const char *path = getenv("SL_PATH");
+        const bool direct = vec && path && strcmp(path, "direct") == 0;
+        TileCfg cfg{};
+        DirectCfg dcfg{};
+        int nt, tm;
+        if (direct) {
+            dcfg = choose_direct_cfg(a.m, w);
+            nt = dcfg.nt;
+            tm = dcfg.tm();
+        } else {
+            cfg = choose_cfg(a.m, w);
+            nt = cfg.nt();
+            tm = cfg.tm();
+        }
+        a.n_cgroups = (ti.n_tiles + nt - 1) / nt;
         a.om = nullptr;
         for (int i = 0; i < w->dev.n_om; ++i)
-            if (w->dev.om_nt[i] == cfg.nt()) a.om = w->dev.om[i];
+            if (w->dev.om_nt[i] == nt) a.om = w->dev.om[i];
         if (!a.om) {
             set_error("internal: no overflow table for the chosen workgroup shape");
             return SL_ERR_UNSUPPORTED;
         }
-        const int64_t mt = (a.m + cfg.tm() - 1) / cfg.tm();
+        const int64_t mt = (a.m + tm - 1) / tm;
         a.n_items = mt * a.n_cgroups;
         if (a.n_items > 0x7fffffff) {
             set_error("too many work items for one launch");
             return SL_ERR_UNSUPPORTED;
         }
         sl_status st;
-        switch (run_kind) {
-        case SL_EPI_ACC_I32: st = launch_vec<SL_EPI_ACC_I32>(a, nullptr, cfg, s, vec); break;
-        case SL_EPI_F32: st = launch_vec<SL_EPI_F32>(a, nullptr, cfg, s, vec); break;
-        case SL_EPI_F32_GELU: st = launch_vec<SL_EPI_F32_GELU>(a, nullptr, cfg, s, vec); break;
-        case SL_EPI_I8: st = launch_vec<SL_EPI_I8>(a, nullptr, cfg, s, vec); break;
-        case SL_EPI_I8_GELU: st = launch_vec<SL_EPI_I8_GELU>(a, &ga, cfg, s, vec); break;
-        default: st = launch_vec<kEpiI8GeluErf>(a, nullptr, cfg, s, vec); break;
+        if (direct) {
+            st = launch_direct(a, run_kind == SL_EPI_I8_GELU ? &ga : nullptr, run_kind, dcfg, s);
+        } else {
+            switch (run_kind) {
+            case SL_EPI_ACC_I32: st = launch_vec<SL_EPI_ACC_I32>(a, nullptr, cfg, s, vec); break;
+            case SL_EPI_F32: st = launch_vec<SL_EPI_F32>(a, nullptr, cfg, s, vec); break;
+            case SL_EPI_F32_GELU: st = launch_vec<SL_EPI_F32_GELU>(a, nullptr, cfg, s, vec); break;
+            case SL_EPI_I8: st = launch_vec<SL_EPI_I8>(a, nullptr, cfg, s, vec); break;
+            case SL_EPI_I8_GELU: st = launch_vec<SL_EPI_I8_GELU>(a, &ga, cfg, s, vec); break;
+            default: st = launch_vec<kEpiI8GeluErf>(a, nullptr, cfg, s, vec); break;
+            }
         }
         if (st != SL_OK) return st;
     }

@@ -1,0 +1,562 @@
+// The direct-operand kernel of the sparse INT8 linear layer (gfx950): for
+// token rows that are 16-byte aligned (k_in % 16 == 0).
+//
+// Same method and operand image as the staged kernel (Section "Sparse GEMM
+// operators", Figure 1, Algorithm 1: the stored 4x1 blocks are one operand of
+// the 4:2-sparse int8 matrix instruction, the input columns the weight's mask
+// names are selected by the instruction's column indices, int32 accumulation,
+// one fused epilogue per output). What differs is where the dense operand
+// comes from. Each compute wave owns ST 16-token subtiles and all NT channel
+// tiles of the workgroup, so no two waves use the same token rows: a wave
+// loads its B operands (32 bytes of one token row per lane) straight from
+// memory into registers, two windows ahead, and only the weight operands
+// pass through LDS, where all compute waves share them. That halves the LDS
+// traffic of a window and leaves LDS bandwidth to the weight operands.
+//
+// Copy waves stream each window's weight operands into a ring of D LDS
+// buffers: the NT main operands, the overflow mask of the item's tiles, and
+// the overflow operands present in the window, packed (rank order of their
+// tiles) so that only present operands are copied. A copy instruction of the
+// packed region that would hold none is replaced by a one-lane copy, which
+// keeps the number of copies per window fixed for the waits that count them.
+// Work items (token tile x channel group) are spread over a persistent grid.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <type_traits>
+
+#include "sl_device.h"
+
+namespace sl {
+
+// Workgroup shape: WM compute waves along the tokens, each with ST 16-token
+// subtiles x all NT 16-channel tiles; as many copy waves; D windows in flight.
+// One window's buffer: NT main operands, then up to NT packed overflow
+// operands; each region is padded to whole 64-lane copies per copy wave.
+template <int ST, int NT, int WM, int D>
+struct DShape {
+    static constexpr int NW = WM;
+    static constexpr int NTH = 64 * NW;                          // lanes of the compute (and of the copy) waves
+    static constexpr int NTHG = 2 * NTH;                         // threads per workgroup
+    static constexpr int TM = 16 * ST * WM;                      // tokens per work item
+    static constexpr int CA = (NT * kOpPieces + NTH - 1) / NTH;  // copies per copy wave per region
+    static constexpr int AB = CA * NTH * 16;
+    static constexpr int COPIES = 2 * CA + 1;  // per copy wave per window: main, mask, overflow
+    static constexpr int BUF = 2 * AB;
+    static constexpr int LDS = D * BUF;
+    static constexpr int VEC = 2 * NT * kTileN * 4;  // per compute wave: weight scales, then biases
+    static constexpr int MASKS = D * NW * 4;         // per ring buffer and copy wave: the overflow mask
+    static_assert(NT <= 32, "an overflow mask has 32 bits");
+};
+
+template <int KIND, int ST, int NT, int WM, int D>
+__device__ __forceinline__ void direct_body(const LinearArgs &a, const GeluArg *ep)
+{
+    using S = DShape<ST, NT, WM, D>;
+    extern __shared__ __attribute__((aligned(16))) int8_t smem[];
+
+    const int tid = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int lane = tid & 63;
+    // waves 0..NW-1 load the token rows and run the matrix instructions;
+    // waves NW..2NW-1 only copy weight operands
+    const bool copier = wave >= S::NW;
+    const int pw = copier ? wave - S::NW : 0;
+
+    const int32_t G = (int32_t)gridDim.x;
+    const int32_t slot = (int32_t)xcd_work_index(blockIdx.x, G);
+    const int n_my = (int)((a.n_items - slot + G - 1) / G);  // >= 1: the grid is at most n_items
+    const int64_t steps = (int64_t)n_my * a.n_win;
+    const ItemIter first = ItemIter::start(slot, G, a.n_cgroups, a.n_win);
+    auto phys = [&](const ItemIter &it, int w) {
+        const int p = w + it.rot;
+        return p >= a.n_win ? p - a.n_win : p;
+    };
+
+    // LDS: the ring, the GELU table, the compute waves' scales and biases,
+    // the overflow masks
+    GeluCell *tab = reinterpret_cast<GeluCell *>(smem + S::LDS);
+    constexpr int kTabBytes = KIND == SL_EPI_I8_GELU ? kGeluLds : 0;
+    uint32_t *omask = reinterpret_cast<uint32_t *>(smem + S::LDS + kTabBytes + S::NW * S::VEC);
+    float hinv = 0.0f, eoff = 0.0f, cmax = 0.0f;
+    if constexpr (KIND == SL_EPI_I8_GELU) {
+        for (int u = copier ? ep->nc : tid; u < ep->nc; u += S::NTH) tab[u] = ep->cell[u];
+        hinv = ep->hinv;
+        eoff = ep->off;
+        cmax = (float)(ep->nc - 1);
+    }
+
+    // Pipeline over the (item, window) elements, one barrier per element. In
+    // step e the copy waves wait until element e+1 has landed, pass the
+    // barrier and start the copies of element e+D into the buffer of element
+    // e; the compute waves pass the barrier, read element e+1's weight
+    // operands into one register set while element e's matrix instructions
+    // run from the other, start the token-row loads of element e+2, and wait
+    // for their LDS reads before the next barrier.
+    static_assert(D >= 3, "the pipeline reads one element ahead of the one it multiplies");
+    static_assert((D - 1) * S::COPIES < 64, "outstanding copies must fit the 6-bit vector-memory counter");
+
+    if (copier) {
+        typedef const __attribute__((address_space(4))) uint64_t *const_u64_ptr;
+        const const_u64_ptr omt = (const_u64_ptr)(a.om);
+        auto om_at = [&](const ItemIter &it, int pwin) {
+            const uint64_t v = omt[(size_t)pwin * a.n_cgroups + it.cg];
+            return make_uint2((uint32_t)v, (uint32_t)(v >> 32));
+        };
+        const __amdgpu_buffer_rsrc_t mr =
+            __builtin_amdgcn_make_buffer_rsrc((void *)a.main, 0, (int)a.main_bytes, kRsrcWord3);
+        const __amdgpu_buffer_rsrc_t orc =
+            __builtin_amdgcn_make_buffer_rsrc((void *)a.ovf, 0, (int)a.ovf_bytes, kRsrcWord3);
+        const __amdgpu_buffer_rsrc_t omr =
+            __builtin_amdgcn_make_buffer_rsrc((void *)a.om, 0, a.n_win * a.n_cgroups * 8, kRsrcWord3);
+        const uint32_t wstride = (uint32_t)a.n_tiles * kOpBytes;  // main image bytes per window
+        // this lane's piece of each main-operand copy
+        int32_t atile[S::CA], apiece16[S::CA];
+#pragma unroll
+        for (int i = 0; i < S::CA; ++i) {
+            const int piece = (i * S::NW + pw) * 64 + lane;
+            atile[i] = piece / kOpPieces;
+            apiece16[i] = (piece - atile[i] * kOpPieces) * 16;
+        }
+
+        // element cursor (item ic, the kc-th of this workgroup; window wc);
+        // past the last element it repeats the last one
+        ItemIter ic = first;
+        int kc = 0, wc = 0;
+        auto cur_w = [&]() { return phys(ic, kc < n_my ? wc : a.n_win - 1); };
+        uint32_t aoff[S::CA];
+        auto item_offsets = [&]() {
+            const int32_t tile0 = ic.cg * NT;
+            const int32_t ntl = min(NT, a.n_tiles - tile0);
+#pragma unroll
+            for (int i = 0; i < S::CA; ++i)
+                aoff[i] = atile[i] < ntl ? (uint32_t)((tile0 + atile[i]) * kOpBytes + apiece16[i]) : kOob;
+        };
+        auto advance = [&]() {
+            if (++wc == a.n_win) {
+                wc = 0;
+                if (++kc < n_my) {
+                    ic.next();
+                    item_offsets();
+                }
+            }
+        };
+        item_offsets();
+
+        // Copy k (0 <= k < COPIES) of the cursor's element (physical window
+        // w) into ring buffer bi: main operands, the overflow mask (one lane,
+        // 4 bytes), then the packed overflow operands (o: the element's
+        // overflow entry; the item's overflow operands of a window are
+        // consecutive in the image, from index o.y on).
+        constexpr int KM = S::CA;
+        auto copy = [&](int k, int w, int bi, uint2 o) {
+            int8_t *b = smem + bi * S::BUF;
+            if (k < KM) {
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(mr, (lds_void *)(b + (k * S::NW + pw) * 1024), 16, aoff[k],
+                                                         (uint32_t)w * wstride, 0, 0);
+            } else if (k == KM) {
+                if (lane == 0)
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(omr, (lds_void *)(omask + bi * S::NW + pw), 4,
+                                                             (uint32_t)(w * a.n_cgroups + ic.cg) * 8u, 0, 0, 0);
+            } else {
+                const int i = k - KM - 1;
+                const int q0 = (i * S::NW + pw) * 64;  // first packed piece of this copy
+                const int npieces = __builtin_popcount(o.x) * kOpPieces;
+                lds_void *dst = (lds_void *)(b + S::AB + (i * S::NW + pw) * 1024);
+                if (q0 < npieces) {
+                    const int q = q0 + lane;
+                    const uint32_t off = q < npieces ? o.y * (uint32_t)kOpBytes + (uint32_t)q * 16u : kOob;
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(orc, dst, 16, off, 0, 0, 0);
+                } else if (lane == 0) {
+                    // nothing to copy: one lane keeps the count (16 zero bytes
+                    // past the packed operands)
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(orc, dst, 16, kOob, 0, 0, 0);
+                }
+            }
+        };
+
+        // Prologue: the overflow entries of elements 0..D-1 start loading; the
+        // main operands and masks of those elements are copied; a bare
+        // barrier (A) publishes the epilogue table the compute waves filled;
+        // the overflow operands follow; once element 0 has landed a second
+        // barrier (B) publishes it.
+        uint2 o[D];
+        {
+            const ItemIter ic0 = ic;
+            const int kc0 = kc, wc0 = wc;
+#pragma unroll
+            for (int d = 0; d < D; ++d) {
+                o[d] = om_at(ic, cur_w());
+                if (++wc == a.n_win) {
+                    wc = 0;
+                    if (++kc < n_my) ic.next();
+                }
+            }
+            ic = ic0;
+            kc = kc0;
+            wc = wc0;
+        }
+        int wp[D];
+#pragma unroll
+        for (int d = 0; d < D; ++d) {
+            wp[d] = cur_w();
+#pragma unroll
+            for (int k = 0; k <= KM; ++k) copy(k, wp[d], d, make_uint2(0u, 0u));
+            advance();
+        }
+        __builtin_amdgcn_s_barrier();  // (A)
+        asm volatile("" ::: "memory");
+#pragma unroll
+        for (int d = 0; d < D; ++d) {
+#pragma unroll
+            for (int k = KM + 1; k < S::COPIES; ++k) copy(k, wp[d], d, o[d]);
+        }
+        uint2 onx = om_at(ic, cur_w());  // entry of element D
+        wait_vmcnt_le<(D - 1) * S::CA>();  // element 0 landed
+        __builtin_amdgcn_s_barrier();      // (B)
+        asm volatile("" ::: "memory");
+
+        // step e: copies of element e+D into the buffer of element e; the
+        // overflow entry of the next element loads across the next barrier
+        auto cstep = [&](int64_t e, int u) {
+            if (e + 1 < steps) wait_window_landed<D, S::CA, S::COPIES>((int)(e < D ? e : D));
+            // a bare barrier: __syncthreads() would also wait for the later
+            // elements' copies still in flight
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");
+            const int w = cur_w();
+#pragma unroll
+            for (int k = 0; k < S::COPIES; ++k) copy(k, w, u, onx);
+            advance();
+            onx = om_at(ic, cur_w());
+        };
+        int64_t e = 0;
+        for (; e + D <= steps; e += D) {
+#pragma unroll
+            for (int u = 0; u < D; ++u) cstep(e + u, u);
+        }
+#pragma unroll
+        for (int u = 0; u < D; ++u)
+            if (e + u < steps) cstep(e + u, u);
+        __builtin_amdgcn_s_waitcnt(0);  // no copy may land after the workgroup ends
+        return;
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // the epilogue table's LDS stores are done
+    __builtin_amdgcn_s_barrier();   // (A)
+    asm volatile("" ::: "memory");
+
+    // ---- compute waves
+    const int wm = wave;
+    // this lane's index word: block-row (lane%16)/4, lane group lane/16
+    const int iword = ((lane & 15) >> 2) * 4 + (lane >> 4);
+
+    // Token rows: lane l of subtile s loads bytes 32*(l/16) .. +31 of its
+    // window of token row (l % 16) -- the B operand layout. Rows past m read
+    // zeros (out-of-range offsets); a ragged last window reads the next row's
+    // first bytes (or zeros past the buffer), which meet zero weights.
+    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)a.x, 0, (int)min<int64_t>(a.m * a.k, kMaxBufferBytes), kRsrcWord3);
+    auto row_offsets = [&](const ItemIter &it, uint32_t (&ro)[ST]) {
+#pragma unroll
+        for (int s = 0; s < ST; ++s) {
+            const int64_t r = (int64_t)it.mt * S::TM + wm * ST * 16 + s * 16 + (lane & 15);
+            ro[s] = r < a.m ? (uint32_t)(r * a.k) + 32u * (uint32_t)(lane >> 4) : kOob;
+        }
+    };
+    auto load_rows = [&](i32x8 (&bv)[ST], const uint32_t (&ro)[ST], int w) {
+#pragma unroll
+        for (int s = 0; s < ST; ++s) {
+            const uint32_t off = ro[s] + (uint32_t)w * kWin;
+            const i32x4 lo = __builtin_bit_cast(i32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0));
+            const i32x4 hi = __builtin_bit_cast(i32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, off + 16u, 0, 0));
+            bv[s] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        }
+    };
+
+    // Weight operands of one element in registers: main and overflow A
+    // operands with their index words. Two sets alternate (steps e, e+1).
+    struct Ops {
+        i32x4 av[NT], ao[NT];
+        int ix[NT], io[NT];
+    };
+    Ops ops[2];
+    i32x8 bv[2][ST];  // token rows of elements e (set e & 1) and e+1
+    auto read_main = [&](Ops &r, const int8_t *b) {
+#pragma unroll
+        for (int c = 0; c < NT; ++c) {
+            const int8_t *op = b + c * kOpBytes;
+            r.av[c] = *reinterpret_cast<const i32x4 *>(op + lane * 16);
+            r.ix[c] = *reinterpret_cast<const int *>(op + 1024 + iword * 4);
+        }
+    };
+    // overflow operand of tile c, packed at rank j
+    auto read_ovf = [&](Ops &r, const int8_t *b, int c, int j) {
+        const int8_t *oo = b + S::AB + j * kOpBytes;
+        r.ao[c] = *reinterpret_cast<const i32x4 *>(oo + lane * 16);
+        r.io[c] = *reinterpret_cast<const int *>(oo + 1024 + iword * 4);
+    };
+    auto read_mask = [&](int b) { return (uint32_t)__builtin_amdgcn_readfirstlane((int)omask[b * S::NW]); };
+
+    // the item's weight scales and biases, one copy each into this wave's
+    // LDS area (NT*4 lanes of 16 bytes); the epilogue waits for them
+    float *vec = reinterpret_cast<float *>(smem + S::LDS + kTabBytes + wave * S::VEC);
+    auto fetch_vec = [&](const ItemIter &it) {
+        if constexpr (KIND != SL_EPI_ACC_I32) {
+            const __amdgpu_buffer_rsrc_t sr =
+                __builtin_amdgcn_make_buffer_rsrc((void *)a.w_scale, 0, a.n * 4, kRsrcWord3);
+            const __amdgpu_buffer_rsrc_t br = __builtin_amdgcn_make_buffer_rsrc((void *)a.bias, 0, a.n * 4, kRsrcWord3);
+            if (lane < NT * 4) {
+                const uint32_t off = (uint32_t)((it.cg * NT * kTileN + lane * 4) * 4);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(sr, (lds_void *)vec, 16, off, 0, 0, 0);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(br, (lds_void *)(vec + NT * kTileN), 16, off, 0, 0, 0);
+            }
+        }
+    };
+
+    i32x4 acc[NT][ST];
+    auto clear_acc = [&]() {
+#pragma unroll
+        for (int c = 0; c < NT; ++c)
+#pragma unroll
+            for (int s = 0; s < ST; ++s) acc[c][s] = i32x4{0, 0, 0, 0};
+    };
+    // accumulator layout: lane l holds rows 4*(l/16)+r (channels of one
+    // block-row), column l%16 (token), r = 0..3
+    auto epilogue = [&](const ItemIter &it) {
+        __builtin_amdgcn_s_waitcnt(0);  // this wave's scale and bias copies
+        const int64_t t0 = (int64_t)it.mt * S::TM + wm * ST * 16;  // this wave's first token
+        const int32_t tile0 = it.cg * NT;
+        auto scales = [&](int c, float (&s)[4], float (&bb4)[4]) {
+            if constexpr (KIND != SL_EPI_ACC_I32) {
+                const int lc = c * kTileN + 4 * (lane >> 4);
+                const float4 sw = *reinterpret_cast<const float4 *>(vec + lc);
+                const float4 bb = *reinterpret_cast<const float4 *>(vec + NT * kTileN + lc);
+                s[0] = a.sx * sw.x;
+                s[1] = a.sx * sw.y;
+                s[2] = a.sx * sw.z;
+                s[3] = a.sx * sw.w;
+                bb4[0] = bb.x;
+                bb4[1] = bb.y;
+                bb4[2] = bb.z;
+                bb4[3] = bb.w;
+            } else {
+                for (int r = 0; r < 4; ++r) s[r] = bb4[r] = 0.0f;
+            }
+        };
+        if (t0 + ST * 16 <= a.m && (tile0 + NT) * kTileN <= a.n) {
+            // whole tile: a uniform base and a lane offset, no bounds checks
+            using T = typename EpiOut<KIND>::T;
+            constexpr int EB = EpiOut<KIND>::kBytes;
+            int8_t *base = static_cast<int8_t *>(a.y) + (t0 * a.n + (int64_t)tile0 * kTileN) * EB;
+            const uint32_t lo = (uint32_t)(((lane & 15) * a.n + 4 * (lane >> 4)) * EB);
+#pragma unroll
+            for (int c = 0; c < NT; ++c) {
+                float s[4], bb4[4];
+                scales(c, s, bb4);
+#pragma unroll
+                for (int st = 0; st < ST; ++st)
+                    *reinterpret_cast<T *>(base + lo + ((int64_t)st * 16 * a.n + c * kTileN) * EB) =
+                        epilogue_value<KIND>(a, acc[c][st], s, bb4, tab, hinv, eoff, cmax);
+            }
+        } else {
+#pragma unroll
+            for (int c = 0; c < NT; ++c) {
+                const int32_t t = tile0 + c;
+                if (t >= a.n_tiles) break;
+                const int32_t ch0 = t * kTileN + 4 * (lane >> 4);
+                if (ch0 >= a.n) continue;  // block-rows past n_out in the last tile
+                float s[4], bb4[4];
+                scales(c, s, bb4);
+#pragma unroll
+                for (int st = 0; st < ST; ++st)
+                    epilogue_store<KIND>(a, acc[c][st], t0 + st * 16 + (lane & 15), ch0, s, bb4, tab, hinv, eoff,
+                                         cmax);
+            }
+        }
+    };
+
+    // element cursors: the token rows of element e+2 are loaded in step e
+    // (item ib, window wb); sl is element e's ring buffer
+    ItemIter ib = first;
+    int kb = 0, wb = 0;
+    uint32_t rob[ST];
+    row_offsets(ib, rob);
+    auto advance_b = [&]() {
+        if (++wb == a.n_win) {
+            wb = 0;
+            if (++kb < n_my) {
+                ib.next();
+                row_offsets(ib, rob);
+            }
+        }
+    };
+    auto load_next_rows = [&](i32x8 (&dst)[ST]) {
+        load_rows(dst, rob, phys(ib, kb < n_my ? wb : a.n_win - 1));
+        advance_b();
+    };
+    int sl = 0;
+    int64_t e = 0;
+    uint32_t mask_w;  // overflow mask of element e
+    auto step = [&](auto pr) {
+        constexpr int PR = decltype(pr)::value;
+        Ops &cur = ops[PR];
+        Ops &nxt = ops[PR ^ 1];
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        const int sl1 = sl + 1 == D ? 0 : sl + 1;
+        const int8_t *nb = smem + sl1 * S::BUF;
+        // Main part: element e+1's main operand reads and element e's main
+        // matrix instructions, one after the other. Products of tiles past
+        // the item's last tile land in accumulators that are never stored.
+        read_main(nxt, nb);
+#pragma unroll
+        for (int c = 0; c < NT; ++c)
+#pragma unroll
+            for (int s = 0; s < ST; ++s)
+                acc[c][s] =
+                    __builtin_amdgcn_smfmac_i32_16x16x128_i8(cur.av[c], bv[PR][s], acc[c][s], cur.ix[c], 0, 0);
+#pragma unroll
+        for (int v = 0; v < NT * ST; ++v) {
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one matrix instruction
+        }
+        __builtin_amdgcn_sched_group_barrier(0x100, 2 * NT, 0);  // the remaining reads
+        // element e+1's overflow mask, read once the main matrix instructions
+        // are queued (its latency hides behind them)
+        __builtin_amdgcn_sched_barrier(0);
+        const uint32_t mask_n = read_mask(sl1);
+        // overflow part, per tile (packed operands: rank = set bits below)
+#pragma unroll
+        for (int c = 0; c < NT; ++c) {
+            if (e + 1 < steps && ((mask_n >> c) & 1u))
+                read_ovf(nxt, nb, c, __builtin_popcount(mask_n & ((1u << c) - 1u)));
+            if ((mask_w >> c) & 1u) {
+#pragma unroll
+                for (int s = 0; s < ST; ++s)
+                    acc[c][s] =
+                        __builtin_amdgcn_smfmac_i32_16x16x128_i8(cur.ao[c], bv[PR][s], acc[c][s], cur.io[c], 0, 0);
+            }
+        }
+        // element e's token rows are consumed: load element e+2's into the set
+        load_next_rows(bv[PR]);
+        // element e+1's buffer is refilled after the next barrier: its reads
+        // must be done by then
+        wait_lgkm0();
+        mask_w = mask_n;
+        sl = sl1;
+        ++e;
+    };
+    using P0 = std::integral_constant<int, 0>;
+    using P1 = std::integral_constant<int, 1>;
+
+    ItemIter it = first;
+    clear_acc();
+    fetch_vec(it);
+    load_next_rows(bv[0]);
+    load_next_rows(bv[1]);
+    __builtin_amdgcn_s_barrier();  // (B): element 0 has landed
+    asm volatile("" ::: "memory");
+    mask_w = read_mask(0);
+    read_main(ops[0], smem);
+#pragma unroll
+    for (int c = 0; c < NT; ++c)
+        if ((mask_w >> c) & 1u) read_ovf(ops[0], smem, c, __builtin_popcount(mask_w & ((1u << c) - 1u)));
+    wait_lgkm0();  // element 0's buffer is refilled after the next barrier
+    // Each item starts with its first element's operands in set 0; after an
+    // odd number of windows they are moved there from set 1.
+    for (int k = 0; k < n_my; ++k) {
+        int w = 0;
+        for (; w + 2 <= a.n_win; w += 2) {
+            step(P0{});
+            step(P1{});
+        }
+        if (w < a.n_win) {
+            step(P0{});
+            ops[0] = ops[1];
+#pragma unroll
+            for (int s = 0; s < ST; ++s) {
+                const i32x8 t = bv[0][s];
+                bv[0][s] = bv[1][s];
+                bv[1][s] = t;
+            }
+        }
+        epilogue(it);
+        if (k + 1 < n_my) {
+            clear_acc();
+            it.next();
+            asm volatile("" ::: "memory");  // the epilogue's reads of the scales come first
+            fetch_vec(it);
+        }
+    }
+}
+
+template <int KIND, int ST, int NT, int WM, int D>
+__global__ __launch_bounds__(128 * WM) void sparse_linear_direct_kernel(LinearArgs a)
+{
+    direct_body<KIND, ST, NT, WM, D>(a, nullptr);
+}
+
+template <int ST, int NT, int WM, int D>
+__global__ __launch_bounds__(128 * WM) void sparse_linear_direct_gelu_kernel(LinearArgs a, GeluArg ep)
+{
+    direct_body<SL_EPI_I8_GELU, ST, NT, WM, D>(a, &ep);
+}
+
+template <int KIND, int ST, int NT, int WM, int D>
+static sl_status launch_direct_cfg(const LinearArgs &a, const GeluArg *ep, hipStream_t stream)
+{
+    using S = DShape<ST, NT, WM, D>;
+    const void *fn;
+    if constexpr (KIND == SL_EPI_I8_GELU)
+        fn = reinterpret_cast<const void *>(&sparse_linear_direct_gelu_kernel<ST, NT, WM, D>);
+    else
+        fn = reinterpret_cast<const void *>(&sparse_linear_direct_kernel<KIND, ST, NT, WM, D>);
+    const size_t lds = (size_t)S::LDS + S::NW * S::VEC + S::MASKS + (KIND == SL_EPI_I8_GELU ? kGeluLds : 0);
+    static_assert(S::LDS + S::NW * S::VEC + S::MASKS + kGeluLds <= kLdsMax, "workgroup shape exceeds LDS");
+    static int resident[kMaxDevices] = {};  // per kernel instance and device
+    int grid = 0;
+    const sl_status st = persistent_grid(fn, S::NTHG, lds, resident, &grid);
+    if (st != SL_OK) return st;
+    const int64_t nwg = std::min<int64_t>(a.n_items, grid);
+    if constexpr (KIND == SL_EPI_I8_GELU)
+        hipLaunchKernelGGL((sparse_linear_direct_gelu_kernel<ST, NT, WM, D>), dim3((uint32_t)nwg), dim3(S::NTHG), lds,
+                           stream, a, *ep);
+    else
+        hipLaunchKernelGGL((sparse_linear_direct_kernel<KIND, ST, NT, WM, D>), dim3((uint32_t)nwg), dim3(S::NTHG),
+                           lds, stream, a);
+    HIP_TRY(hipGetLastError());
+    return SL_OK;
+}
+
+template <int KIND>
+static sl_status launch_direct_kind(const LinearArgs &a, const GeluArg *ep, DirectCfg c, hipStream_t stream)
+{
+#define SL_DCFG(A_, B_, C_, D_) \
+    if (c.st == A_ && c.nt == B_ && c.wm == C_ && c.d == D_) return launch_direct_cfg<KIND, A_, B_, C_, D_>(a, ep, stream);
+    SL_DCFG(2, 6, 4, 4)
+    SL_DCFG(1, 6, 4, 6)
+    SL_DCFG(1, 2, 4, 8)
+#undef SL_DCFG
+    set_error("internal: unknown direct workgroup shape");
+    return SL_ERR_UNSUPPORTED;
+}
+
+const DirectCfg kDirectCfgs[kNumDirectCfgs] = {
+    {2, 6, 4, 4},  // 128 tokens x 96 channels
+    {1, 6, 4, 6},  //  64 tokens x 96 channels
+    {1, 2, 4, 8},  //  64 tokens x 32 channels (few work items)
+};
+
+sl_status launch_direct(const LinearArgs &a, const GeluArg *ep, int32_t run_kind, DirectCfg c, hipStream_t stream)
+{
+    switch (run_kind) {
+    case SL_EPI_ACC_I32: return launch_direct_kind<SL_EPI_ACC_I32>(a, nullptr, c, stream);
+    case SL_EPI_F32: return launch_direct_kind<SL_EPI_F32>(a, nullptr, c, stream);
+    case SL_EPI_F32_GELU: return launch_direct_kind<SL_EPI_F32_GELU>(a, nullptr, c, stream);
+    case SL_EPI_I8: return launch_direct_kind<SL_EPI_I8>(a, nullptr, c, stream);
+    case SL_EPI_I8_GELU: return launch_direct_kind<SL_EPI_I8_GELU>(a, ep, c, stream);
+    default: return launch_direct_kind<kEpiI8GeluErf>(a, nullptr, c, stream);
+    }
+}
+
+}  // namespace sl

@@ -52,7 +52,7 @@ struct TileImage {
 
 // Step table of the fused GELU(erf) + int8 requantisation (gelu_table.cpp).
 constexpr int kGeluCells = 448;
-struct GeluCell {
+struct alignas(8) GeluCell {
     float thr;     // first y of the cell whose code is q_hi (+inf: none)
     int8_t q_lo;   // code of the cell's y below thr
     int8_t q_hi;   // code from thr on

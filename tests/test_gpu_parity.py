@@ -68,12 +68,25 @@ SMALL = [(1, 4, 1), (3, 16, 7), (16, 16, 64), (17, 20, 100), (64, 48, 768), (65,
          (33, 32, 3072), (130, 1024, 4096), (5, 12, 2049)]
 
 
+# kernel paths: the default choice (the staged kernel for row-major token
+# rows) and the direct-operand kernel in each of its workgroup shapes
+PATHS = {"default": {}, "direct": {"SL_PATH": "direct"},
+         "direct_64x96": {"SL_PATH": "direct", "SL_DTILE": "1,6,4,6"},
+         "direct_64x32": {"SL_PATH": "direct", "SL_DTILE": "1,2,4,8"},
+         "direct_128x96": {"SL_PATH": "direct", "SL_DTILE": "2,6,4,4"}}
+
+
 @pytest.mark.parametrize("m,n,k", SMALL)
 @pytest.mark.parametrize("density", [0.0, 0.1, 0.35, 1.0])
-def test_small_shapes_all_kinds(hip, m, n, k, density):
+@pytest.mark.parametrize("path", list(PATHS))
+def test_small_shapes_all_kinds(hip, monkeypatch, m, n, k, density, path):
+    if path != "default" and density in (0.0, 1.0):
+        pytest.skip("the extreme densities run on the default path only")
+    for key, val in PATHS[path].items():
+        monkeypatch.setenv(key, val)
     w, sw, b, rng = _case(n, k, density, 1000 * m + 10 * n + k + int(density * 100))
     x = rng.integers(-127, 128, (m, k), dtype=np.int8)
-    say(f"small m={m} n={n} k={k} d={density}")
+    say(f"small m={m} n={n} k={k} d={density} path={path}")
     pw = hip.PackedWeight.pack(w, sw, b)
     for name, kind in KINDS.items():
         so = 1.0
