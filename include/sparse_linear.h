@@ -9,7 +9,8 @@
  * downconvert; Appendix "Graph optimization" and Algorithm 1's
  * "downconvert and post-operator fusion").
  *
- * Shapes and layouts (all row-major, contiguous):
+ * Shapes and layouts (row-major and contiguous unless a call takes an
+ * sl_layout, below):
  *   X  [m_tokens x k_in]   int8, device memory     (tokens x input features)
  *   W  [n_out    x k_in]   int8, host memory       (output x input features)
  *   Y  [m_tokens x n_out]  int32 | fp32 | int8, device memory, per epilogue
@@ -36,7 +37,7 @@
 extern "C" {
 #endif
 
-#define SL_ABI_VERSION 1
+#define SL_ABI_VERSION 2
 
 typedef enum {
     SL_OK = 0,
@@ -55,6 +56,29 @@ typedef enum {
     SL_EPI_I8 = 3,      /* dequant + bias -> requantised int8                   */
     SL_EPI_I8_GELU = 4  /* dequant + bias + GELU(erf) -> requantised int8       */
 } sl_epilogue_kind;
+
+/*
+ * Layouts of an int8 activation tensor of `rows` tokens x `cols` features
+ * (the input X of a layer, or the int8 output Y that feeds the next layer):
+ *   SL_LAYOUT_ROWS    row-major: element (t, c) at byte t * cols + c.
+ *   SL_LAYOUT_T16X32  blocks of 16 tokens x 32 features, each block 512
+ *                     contiguous bytes, token-major inside: element (t, c) at
+ *                     byte ((t / 16) * C + c / 32) * 512 + (t % 16) * 32 + c % 32
+ *                     with C = ceil(cols / 32); the tensor occupies
+ *                     ceil(rows / 16) * C * 512 bytes. Bytes of padding
+ *                     tokens (t >= rows) and padding features (c >= cols)
+ *                     may hold anything: a layer never lets them reach a
+ *                     stored output (padding features meet zero weights).
+ * T16X32 is the order in which the matrix cores consume the dense operand
+ * (16 tokens per instruction, 32 consecutive features per lane), so a layer
+ * reads it with whole cache lines per group of lanes; a chain of layers can
+ * keep its activations in it from the first quantisation to the last
+ * int8 output.
+ */
+typedef enum {
+    SL_LAYOUT_ROWS = 0,
+    SL_LAYOUT_T16X32 = 1
+} sl_layout;
 
 /* Opaque packed weight. Immutable after packing: any number of threads and
  * streams may run with one handle at once (the paper's weight sharing across
@@ -119,6 +143,22 @@ sl_status sparse_linear_run(const sl_packed_weight *w, const int8_t *x_dev, int6
                             void *hip_stream);
 
 /*
+ * sparse_linear_run with explicit activation layouts (sl_layout):
+ *   x_layout      layout of x_dev (rows = m_tokens, cols = k_in). For
+ *                 SL_LAYOUT_T16X32 x_dev must be 16-byte aligned.
+ *   y_layout      layout of y_dev (rows = m_tokens, cols = n_out).
+ *                 SL_LAYOUT_T16X32 only for SL_EPI_I8 / SL_EPI_I8_GELU, with
+ *                 y_dev 16-byte aligned; it writes every real (token,
+ *                 channel) byte, padding bytes are left unspecified.
+ * Other arguments, results and errors as sparse_linear_run, which is this
+ * call with both layouts SL_LAYOUT_ROWS. Bad layout values or alignment:
+ * SL_ERR_INVALID_ARG.
+ */
+sl_status sparse_linear_run_layout(const sl_packed_weight *w, const int8_t *x_dev, int32_t x_layout,
+                                   int64_t m_tokens, float x_scale, int32_t epilogue_kind, float out_scale,
+                                   void *y_dev, int32_t y_layout, void *hip_stream);
+
+/*
  * Per-tensor symmetric activation quantisation for the first op of a chain
  * (Section "Post-training quantization"): q = clamp(rint(x * (1/scale)), -127, 127)
  * with fl(1/scale) computed once in fp32. Asynchronous on hip_stream.
@@ -128,6 +168,16 @@ sl_status sparse_linear_run(const sl_packed_weight *w, const int8_t *x_dev, int6
  *   q_dev  [numel] int8 device pointer, must not overlap x_dev
  */
 sl_status quantize_act(const float *x_dev, int64_t numel, float scale, int8_t *q_dev, void *hip_stream);
+
+/*
+ * quantize_act of a [rows x cols] fp32 row-major tensor into q_layout
+ * (sl_layout). SL_LAYOUT_ROWS is quantize_act of rows * cols elements; for
+ * SL_LAYOUT_T16X32 q_dev (16-byte aligned) receives ceil(rows/16) *
+ * ceil(cols/32) * 512 bytes, padding bytes written as 0. rows, cols >= 0
+ * (either 0: no-op); x_dev 4-byte aligned.
+ */
+sl_status quantize_act_layout(const float *x_dev, int64_t rows, int32_t cols, float scale, int8_t *q_dev,
+                              int32_t q_layout, void *hip_stream);
 
 /* Rebuild the dense [n_out x k_in] int8 weight from the handle's GPU tile
  * image (host mirror), into caller memory w_host. Round trip of the packer. */

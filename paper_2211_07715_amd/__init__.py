@@ -8,6 +8,15 @@ PyTorch fallback: if the shared library is missing, ``load()`` raises.
     pw = sl.PackedWeight.pack(w_int8, w_scale, bias)        # host -> device, once
     q = sl.quantize_act(x_f32_cuda, x_scale)                 # first op of a chain
     y = pw.run(q, x_scale, sl.EPI_I8_GELU, out_scale=so)     # int8 [M, N]
+
+Activations between layers can stay in the 16-token x 32-feature block layout
+(LAYOUT_T16X32, 4-D tensors [ceil(M/16), ceil(C/32), 16, 32]), the order the
+matrix cores read them in:
+
+    q = sl.quantize_act(x_f32_cuda, x_scale, layout=sl.LAYOUT_T16X32)
+    h = pw1.run(q, x_scale, sl.EPI_I8_GELU, out_scale=so, m_tokens=M,
+                x_layout=sl.LAYOUT_T16X32, y_layout=sl.LAYOUT_T16X32)
+    y = pw2.run(h, so, sl.EPI_F32, m_tokens=M, x_layout=sl.LAYOUT_T16X32)   # fp32 [M, N2]
 """
 from __future__ import annotations
 
@@ -22,13 +31,15 @@ LIB_PATH = os.path.join(HERE, "libsparse_linear.so")
 
 EPI_ACC_I32, EPI_F32, EPI_F32_GELU, EPI_I8, EPI_I8_GELU = 0, 1, 2, 3, 4
 EPI_BY_NAME = {"acc_i32": 0, "f32": 1, "f32_gelu": 2, "i8": 3, "i8_gelu": 4}
+LAYOUT_ROWS, LAYOUT_T16X32 = 0, 1
 
 SL_OK = 0
 STATUS = {0: "SL_OK", -1: "SL_ERR_INVALID_ARG", -2: "SL_ERR_SHAPE", -3: "SL_ERR_HIP", -4: "SL_ERR_OOM",
           -5: "SL_ERR_UNSUPPORTED", -6: "SL_ERR_NOT_ON_DEVICE"}
 
 # every symbol include/sparse_linear.h declares
-EXPORTS = ("sparse_linear_pack", "sparse_linear_pack_host", "sparse_linear_run", "quantize_act",
+EXPORTS = ("sparse_linear_pack", "sparse_linear_pack_host", "sparse_linear_run", "sparse_linear_run_layout",
+           "quantize_act", "quantize_act_layout",
            "sparse_linear_unpack", "sparse_linear_info", "sparse_linear_export_bsr",
            "sparse_linear_tile_stats", "sparse_linear_free", "sl_status_string", "sl_last_error",
            "sl_abi_version")
@@ -55,12 +66,15 @@ def load() -> ctypes.CDLL:
     lib.sparse_linear_pack.argtypes = [vp, i32, i32, i32, i32, vp, vp, pp]
     lib.sparse_linear_pack_host.argtypes = [vp, i32, i32, i32, i32, vp, vp, pp]
     lib.sparse_linear_run.argtypes = [vp, vp, i64, f32, i32, f32, vp, vp]
+    lib.sparse_linear_run_layout.argtypes = [vp, vp, i32, i64, f32, i32, f32, vp, i32, vp]
     lib.quantize_act.argtypes = [vp, i64, f32, vp, vp]
+    lib.quantize_act_layout.argtypes = [vp, i64, i32, f32, vp, i32, vp]
     lib.sparse_linear_unpack.argtypes = [vp, vp]
     lib.sparse_linear_info.argtypes = [vp, vp, vp, vp]
     lib.sparse_linear_export_bsr.argtypes = [vp, vp, vp, vp]
     lib.sparse_linear_tile_stats.argtypes = [vp, vp, vp, vp, vp]
-    for name in ("sparse_linear_pack", "sparse_linear_pack_host", "sparse_linear_run", "quantize_act",
+    for name in ("sparse_linear_pack", "sparse_linear_pack_host", "sparse_linear_run", "sparse_linear_run_layout",
+                 "quantize_act", "quantize_act_layout",
                  "sparse_linear_unpack", "sparse_linear_info", "sparse_linear_export_bsr",
                  "sparse_linear_tile_stats"):
         getattr(lib, name).restype = i32
@@ -84,6 +98,26 @@ def _check(status: int, where: str):
 
 def _np_ptr(a: Optional[np.ndarray]):
     return None if a is None else ctypes.c_void_p(a.ctypes.data)
+
+
+def t16x32_shape(rows: int, cols: int):
+    """Shape of a [rows x cols] activation in LAYOUT_T16X32."""
+    return ((rows + 15) // 16, (cols + 31) // 32, 16, 32)
+
+
+def to_t16x32(a: np.ndarray, fill: int = 0) -> np.ndarray:
+    """Host copy of an int8 [rows x cols] array in LAYOUT_T16X32 (padding = fill)."""
+    rows, cols = a.shape
+    rb, cb, _, _ = t16x32_shape(rows, cols)
+    p = np.full((rb * 16, cb * 32), fill, dtype=a.dtype)
+    p[:rows, :cols] = a
+    return np.ascontiguousarray(p.reshape(rb, 16, cb, 32).transpose(0, 2, 1, 3))
+
+
+def from_t16x32(b: np.ndarray, rows: int, cols: int) -> np.ndarray:
+    """The [rows x cols] array held by a LAYOUT_T16X32 array (padding dropped)."""
+    rb, cb, _, _ = b.shape
+    return np.ascontiguousarray(b.transpose(0, 2, 1, 3).reshape(rb * 16, cb * 32)[:rows, :cols])
 
 
 def _stream_ptr(stream) -> Optional[int]:
@@ -165,35 +199,68 @@ class PackedWeight:
                                                ctypes.byref(ib)), "sparse_linear_tile_stats")
         return {"n_tiles": nt.value, "n_entries": ne.value, "n_overflow": no.value, "image_bytes": ib.value}
 
-    def run(self, x, x_scale: float, kind: int, out_scale: float = 1.0, out=None, stream=None):
-        """Y = epilogue(X W^T) for a CUDA int8 tensor x [M, k_in]; returns Y."""
+    def run(self, x, x_scale: float, kind: int, out_scale: float = 1.0, out=None, stream=None,
+            x_layout: int = LAYOUT_ROWS, y_layout: int = LAYOUT_ROWS, m_tokens: Optional[int] = None):
+        """Y = epilogue(X W^T) for a CUDA int8 tensor x; returns Y.
+
+        x: [M, k_in] (LAYOUT_ROWS) or t16x32_shape(M, k_in) with m_tokens=M
+        (LAYOUT_T16X32). Y: [M, n_out] of the kind's dtype, or, for the int8
+        kinds with y_layout=LAYOUT_T16X32, t16x32_shape(M, n_out) int8."""
         import torch
-        if x.dtype != torch.int8 or x.dim() != 2 or x.shape[1] != self.k_in or not x.is_cuda:
-            raise ValueError(f"x must be a CUDA int8 tensor [M, {self.k_in}]")
-        if not x.is_contiguous():
-            raise ValueError("x must be contiguous")
+        if x.dtype != torch.int8 or not x.is_cuda or not x.is_contiguous():
+            raise ValueError("x must be a contiguous CUDA int8 tensor")
+        if x_layout == LAYOUT_ROWS:
+            if x.dim() != 2 or x.shape[1] != self.k_in:
+                raise ValueError(f"x must be [M, {self.k_in}]")
+            m = x.shape[0] if m_tokens is None else int(m_tokens)
+            if m != x.shape[0]:
+                raise ValueError("m_tokens differs from x's rows")
+        elif x_layout == LAYOUT_T16X32:
+            if m_tokens is None:
+                raise ValueError("m_tokens is required with LAYOUT_T16X32 input")
+            m = int(m_tokens)
+            if tuple(x.shape) != t16x32_shape(m, self.k_in):
+                raise ValueError(f"x must have shape {t16x32_shape(m, self.k_in)}")
+        else:
+            raise ValueError(f"unknown x_layout {x_layout}")
         dt = {EPI_ACC_I32: torch.int32, EPI_F32: torch.float32, EPI_F32_GELU: torch.float32,
               EPI_I8: torch.int8, EPI_I8_GELU: torch.int8}[kind]
-        m = x.shape[0]
+        shape = t16x32_shape(m, self.n_out) if y_layout == LAYOUT_T16X32 else (m, self.n_out)
         if out is None:
-            out = torch.empty((m, self.n_out), dtype=dt, device=x.device)
-        elif out.dtype != dt or tuple(out.shape) != (m, self.n_out) or not out.is_contiguous():
+            out = torch.empty(shape, dtype=dt, device=x.device)
+        elif out.dtype != dt or tuple(out.shape) != tuple(shape) or not out.is_contiguous():
             raise ValueError("out has the wrong dtype/shape or is not contiguous")
-        _check(load().sparse_linear_run(self.handle, ctypes.c_void_p(x.data_ptr()), m, float(x_scale), int(kind),
-                                        float(out_scale), ctypes.c_void_p(out.data_ptr()), _stream_ptr(stream)),
-               "sparse_linear_run")
+        _check(load().sparse_linear_run_layout(self.handle, ctypes.c_void_p(x.data_ptr()), int(x_layout), m,
+                                               float(x_scale), int(kind), float(out_scale),
+                                               ctypes.c_void_p(out.data_ptr()), int(y_layout), _stream_ptr(stream)),
+               "sparse_linear_run_layout")
         return out
 
 
-def quantize_act(x, scale: float, out=None, stream=None):
-    """q = clamp(rint(x / scale), -127, 127) for a contiguous CUDA fp32 tensor."""
+def quantize_act(x, scale: float, out=None, stream=None, layout: int = LAYOUT_ROWS):
+    """q = clamp(rint(x / scale), -127, 127) for a contiguous CUDA fp32 tensor:
+    same shape (LAYOUT_ROWS), or, for a 2-D x [rows, cols] and
+    layout=LAYOUT_T16X32, int8 of shape t16x32_shape(rows, cols)."""
     import torch
     if x.dtype != torch.float32 or not x.is_cuda or not x.is_contiguous():
         raise ValueError("x must be a contiguous CUDA float32 tensor")
+    if layout == LAYOUT_ROWS:
+        if out is None:
+            out = torch.empty(x.shape, dtype=torch.int8, device=x.device)
+        elif out.dtype != torch.int8 or out.numel() != x.numel() or not out.is_contiguous():
+            raise ValueError("out must be a contiguous int8 tensor with x's size")
+        _check(load().quantize_act(ctypes.c_void_p(x.data_ptr()), x.numel(), float(scale),
+                                   ctypes.c_void_p(out.data_ptr()), _stream_ptr(stream)), "quantize_act")
+        return out
+    if layout != LAYOUT_T16X32 or x.dim() != 2:
+        raise ValueError("LAYOUT_T16X32 quantisation takes a 2-D x [rows, cols]")
+    rows, cols = x.shape
+    shape = t16x32_shape(rows, cols)
     if out is None:
-        out = torch.empty(x.shape, dtype=torch.int8, device=x.device)
-    elif out.dtype != torch.int8 or out.numel() != x.numel() or not out.is_contiguous():
-        raise ValueError("out must be a contiguous int8 tensor with x's size")
-    _check(load().quantize_act(ctypes.c_void_p(x.data_ptr()), x.numel(), float(scale),
-                               ctypes.c_void_p(out.data_ptr()), _stream_ptr(stream)), "quantize_act")
+        out = torch.empty(shape, dtype=torch.int8, device=x.device)
+    elif out.dtype != torch.int8 or tuple(out.shape) != shape or not out.is_contiguous():
+        raise ValueError(f"out must be a contiguous int8 tensor of shape {shape}")
+    _check(load().quantize_act_layout(ctypes.c_void_p(x.data_ptr()), rows, cols, float(scale),
+                                      ctypes.c_void_p(out.data_ptr()), int(layout), _stream_ptr(stream)),
+           "quantize_act_layout")
     return out

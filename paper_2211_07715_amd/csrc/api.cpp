@@ -72,9 +72,9 @@ sl_status sparse_linear_pack_host(const int8_t *w_host, int32_t n_out, int32_t k
 
 static bool good_scale(float s) { return isfinite(s) && s > 0.0f; }
 
-sl_status sparse_linear_run(const sl_packed_weight *w, const int8_t *x_dev, int64_t m_tokens,
-                            float x_scale, int32_t epilogue_kind, float out_scale, void *y_dev,
-                            void *hip_stream)
+sl_status sparse_linear_run_layout(const sl_packed_weight *w, const int8_t *x_dev, int32_t x_layout,
+                                   int64_t m_tokens, float x_scale, int32_t epilogue_kind, float out_scale,
+                                   void *y_dev, int32_t y_layout, void *hip_stream)
 {
     clear_error();
     if (!w) {
@@ -87,6 +87,14 @@ sl_status sparse_linear_run(const sl_packed_weight *w, const int8_t *x_dev, int6
     }
     if (epilogue_kind < SL_EPI_ACC_I32 || epilogue_kind > SL_EPI_I8_GELU) {
         set_error("unknown epilogue kind " + std::to_string(epilogue_kind));
+        return SL_ERR_INVALID_ARG;
+    }
+    if (x_layout != SL_LAYOUT_ROWS && x_layout != SL_LAYOUT_T16X32) {
+        set_error("unknown x_layout " + std::to_string(x_layout));
+        return SL_ERR_INVALID_ARG;
+    }
+    if (y_layout != SL_LAYOUT_ROWS && y_layout != SL_LAYOUT_T16X32) {
+        set_error("unknown y_layout " + std::to_string(y_layout));
         return SL_ERR_INVALID_ARG;
     }
     if (m_tokens < 0) {
@@ -102,19 +110,36 @@ sl_status sparse_linear_run(const sl_packed_weight *w, const int8_t *x_dev, int6
         set_error("out_scale must be finite and > 0 for the int8 epilogues");
         return SL_ERR_INVALID_ARG;
     }
+    if (y_layout == SL_LAYOUT_T16X32 && !i8) {
+        set_error("y_layout SL_LAYOUT_T16X32 is for the int8 epilogues only");
+        return SL_ERR_INVALID_ARG;
+    }
     if (m_tokens == 0) return SL_OK;
     if (!x_dev || !y_dev) {
         set_error("x_dev and y_dev must not be NULL");
         return SL_ERR_INVALID_ARG;
     }
-    const uintptr_t need = i8 ? 4 : 16;
+    if (x_layout == SL_LAYOUT_T16X32 && reinterpret_cast<uintptr_t>(x_dev) % 16) {
+        set_error("x_dev must be 16-byte aligned for SL_LAYOUT_T16X32");
+        return SL_ERR_INVALID_ARG;
+    }
+    const uintptr_t need = (i8 && y_layout == SL_LAYOUT_ROWS) ? 4 : 16;
     if (reinterpret_cast<uintptr_t>(y_dev) % need) {
-        set_error("y_dev must be " + std::to_string(need) + "-byte aligned for this epilogue");
+        set_error("y_dev must be " + std::to_string(need) + "-byte aligned for this epilogue and layout");
         return SL_ERR_INVALID_ARG;
     }
     // fl(1/so), one fp32 division, as the definition states
     const float inv_so = i8 ? 1.0f / out_scale : 1.0f;
-    return launch_linear(w, x_dev, m_tokens, x_scale, epilogue_kind, inv_so, y_dev, hip_stream);
+    return launch_linear(w, x_dev, x_layout, m_tokens, x_scale, epilogue_kind, inv_so, y_dev, y_layout,
+                         hip_stream);
+}
+
+sl_status sparse_linear_run(const sl_packed_weight *w, const int8_t *x_dev, int64_t m_tokens,
+                            float x_scale, int32_t epilogue_kind, float out_scale, void *y_dev,
+                            void *hip_stream)
+{
+    return sparse_linear_run_layout(w, x_dev, SL_LAYOUT_ROWS, m_tokens, x_scale, epilogue_kind, out_scale, y_dev,
+                                    SL_LAYOUT_ROWS, hip_stream);
 }
 
 sl_status quantize_act(const float *x_dev, int64_t numel, float scale, int8_t *q_dev, void *hip_stream)
@@ -135,6 +160,36 @@ sl_status quantize_act(const float *x_dev, int64_t numel, float scale, int8_t *q
     }
     const float inv = 1.0f / scale;
     return launch_quantize(x_dev, numel, inv, q_dev, hip_stream);
+}
+
+sl_status quantize_act_layout(const float *x_dev, int64_t rows, int32_t cols, float scale, int8_t *q_dev,
+                              int32_t q_layout, void *hip_stream)
+{
+    clear_error();
+    if (rows < 0 || cols < 0) {
+        set_error("rows and cols must be >= 0");
+        return SL_ERR_SHAPE;
+    }
+    if (q_layout != SL_LAYOUT_ROWS && q_layout != SL_LAYOUT_T16X32) {
+        set_error("unknown q_layout " + std::to_string(q_layout));
+        return SL_ERR_INVALID_ARG;
+    }
+    if (q_layout == SL_LAYOUT_ROWS) return quantize_act(x_dev, rows * (int64_t)cols, scale, q_dev, hip_stream);
+    if (!good_scale(scale)) {
+        set_error("scale must be finite and > 0");
+        return SL_ERR_INVALID_ARG;
+    }
+    if (rows == 0 || cols == 0) return SL_OK;
+    if (!x_dev || !q_dev) {
+        set_error("x_dev and q_dev must not be NULL");
+        return SL_ERR_INVALID_ARG;
+    }
+    if (reinterpret_cast<uintptr_t>(q_dev) % 16 || reinterpret_cast<uintptr_t>(x_dev) % 4) {
+        set_error("q_dev must be 16-byte and x_dev 4-byte aligned for SL_LAYOUT_T16X32");
+        return SL_ERR_INVALID_ARG;
+    }
+    const float inv = 1.0f / scale;
+    return launch_quantize_t16x32(x_dev, rows, cols, inv, q_dev, hip_stream);
 }
 
 sl_status sparse_linear_unpack(const sl_packed_weight *w, int8_t *w_host)

@@ -77,7 +77,7 @@ __device__ __forceinline__ int xsw(int r) { return (r ^ (r >> 3)) & 7; }
 
 // VEC: X rows are 16-byte aligned and k % 16 == 0, so token rows are copied
 // to LDS with 16-byte direct loads; otherwise they are staged byte by byte.
-template <int KIND, int ST, int CT, int WM, int WN, int D, bool VEC>
+template <int KIND, int ST, int CT, int WM, int WN, int D, bool VEC, bool YT>
 __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const GeluArg *ep)
 {
     using S = Shape<ST, CT, WM, WN, D>;
@@ -433,7 +433,7 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
             }
 #pragma unroll
             for (int st = 0; st < ST; ++st)
-                epilogue_store<KIND>(a, acc[c][st], m0 + wm * ST * 16 + st * 16 + (lane & 15), ch0, s, bb4, tab, hinv,
+                epilogue_store<KIND, YT>(a, acc[c][st], m0 + wm * ST * 16 + st * 16 + (lane & 15), ch0, s, bb4, tab, hinv,
                                      eoff, cmax);
         }
     };
@@ -528,16 +528,16 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
     }
 }
 
-template <int KIND, int ST, int CT, int WM, int WN, int D, bool VEC>
+template <int KIND, int ST, int CT, int WM, int WN, int D, bool VEC, bool YT>
 __global__ __launch_bounds__(128 * WM * WN) void sparse_linear_kernel(LinearArgs a)
 {
-    sparse_linear_body<KIND, ST, CT, WM, WN, D, VEC>(a, nullptr);
+    sparse_linear_body<KIND, ST, CT, WM, WN, D, VEC, YT>(a, nullptr);
 }
 
-template <int ST, int CT, int WM, int WN, int D, bool VEC>
+template <int ST, int CT, int WM, int WN, int D, bool VEC, bool YT>
 __global__ __launch_bounds__(128 * WM * WN) void sparse_linear_gelu_kernel(LinearArgs a, GeluArg ep)
 {
-    sparse_linear_body<SL_EPI_I8_GELU, ST, CT, WM, WN, D, VEC>(a, &ep);
+    sparse_linear_body<SL_EPI_I8_GELU, ST, CT, WM, WN, D, VEC, YT>(a, &ep);
 }
 
 // ---------------------------------------------------------------------------
@@ -569,6 +569,41 @@ __global__ __launch_bounds__(256) void quantize_scalar_kernel(const float *x, in
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
         q[i] = (int8_t)requant_i8(x[i], inv);
+}
+
+// Quantisation into the 16-token x 32-feature block layout: thread j writes
+// 16-byte piece j of the output (block j / 32; token (j % 32) / 2 of the
+// block, features 16 * (j % 2) .. +15 of the block's 32), zeros for padding.
+// VEC: cols % 4 == 0 and x 16-byte aligned, so whole pieces load as float4.
+template <bool VEC>
+__global__ __launch_bounds__(256) void quantize_t16x32_kernel(const float *x, int64_t rows, int32_t cols,
+                                                              int32_t cblocks, int64_t n_pieces, float inv,
+                                                              int8_t *q)
+{
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < n_pieces; j += stride) {
+        const int64_t b = j >> 5;
+        const int w = (int)(j & 31);
+        const int64_t t = (b / cblocks) * 16 + (w >> 1);
+        const int32_t c0 = (int32_t)(b % cblocks) * 32 + (w & 1) * 16;
+        uint4 o = {0u, 0u, 0u, 0u};
+        if (t < rows) {
+            const float *row = x + t * cols;
+            if (VEC && c0 + 16 <= cols) {
+                const float4 *src = reinterpret_cast<const float4 *>(row + c0);
+                o.x = quant4(src[0], inv);
+                o.y = quant4(src[1], inv);
+                o.z = quant4(src[2], inv);
+                o.w = quant4(src[3], inv);
+            } else {
+                uint32_t v[4] = {0u, 0u, 0u, 0u};
+                for (int i = 0; i < 16 && c0 + i < cols; ++i)
+                    v[i >> 2] |= ((uint32_t)requant_i8(row[c0 + i], inv) & 0xffu) << (8 * (i & 3));
+                o = make_uint4(v[0], v[1], v[2], v[3]);
+            }
+        }
+        reinterpret_cast<uint4 *>(q)[j] = o;
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -716,15 +751,15 @@ sl_status persistent_grid(const void *fn, int threads, size_t lds, int *cache, i
     return SL_OK;
 }
 
-template <int KIND, int ST, int CT, int WM, int WN, int D, bool VEC>
+template <int KIND, int ST, int CT, int WM, int WN, int D, bool VEC, bool YT>
 static sl_status launch_cfg(const LinearArgs &a, const GeluArg *ep, hipStream_t stream)
 {
     using S = Shape<ST, CT, WM, WN, D>;
     const void *fn;
     if constexpr (KIND == SL_EPI_I8_GELU)
-        fn = reinterpret_cast<const void *>(&sparse_linear_gelu_kernel<ST, CT, WM, WN, D, VEC>);
+        fn = reinterpret_cast<const void *>(&sparse_linear_gelu_kernel<ST, CT, WM, WN, D, VEC, YT>);
     else
-        fn = reinterpret_cast<const void *>(&sparse_linear_kernel<KIND, ST, CT, WM, WN, D, VEC>);
+        fn = reinterpret_cast<const void *>(&sparse_linear_kernel<KIND, ST, CT, WM, WN, D, VEC, YT>);
     const size_t lds = (size_t)S::LDS + S::NW * kVecLds + kMaskLds + (KIND == SL_EPI_I8_GELU ? kGeluLds : 0);
     static_assert(S::LDS + S::NW * kVecLds + kMaskLds + kGeluLds <= kLdsMax, "workgroup shape exceeds LDS");
     static_assert(D * S::NW * 4 <= kMaskLds, "one overflow mask per ring buffer and copy wave");
@@ -736,34 +771,45 @@ static sl_status launch_cfg(const LinearArgs &a, const GeluArg *ep, hipStream_t 
     if (st != SL_OK) return st;
     const int64_t nwg = std::min<int64_t>(a.n_items, grid);
     if constexpr (KIND == SL_EPI_I8_GELU)
-        hipLaunchKernelGGL((sparse_linear_gelu_kernel<ST, CT, WM, WN, D, VEC>), dim3((uint32_t)nwg), dim3(S::NTHG),
+        hipLaunchKernelGGL((sparse_linear_gelu_kernel<ST, CT, WM, WN, D, VEC, YT>), dim3((uint32_t)nwg), dim3(S::NTHG),
                            lds, stream, a, *ep);
     else
-        hipLaunchKernelGGL((sparse_linear_kernel<KIND, ST, CT, WM, WN, D, VEC>), dim3((uint32_t)nwg), dim3(S::NTHG),
+        hipLaunchKernelGGL((sparse_linear_kernel<KIND, ST, CT, WM, WN, D, VEC, YT>), dim3((uint32_t)nwg), dim3(S::NTHG),
                            lds, stream, a);
     HIP_TRY(hipGetLastError());
     return SL_OK;
 }
 
-template <int KIND, bool VEC>
+template <int KIND, bool VEC, bool YT>
 static sl_status launch_kind(const LinearArgs &a, const GeluArg *ep, TileCfg c, hipStream_t stream)
 {
 #define SL_CFG(A_, B_, C_, D_, E_)                                         \
     if (c.st == A_ && c.ct == B_ && c.wm == C_ && c.wn == D_ && c.d == E_) \
-        return launch_cfg<KIND, A_, B_, C_, D_, E_, VEC>(a, ep, stream);
+        return launch_cfg<KIND, A_, B_, C_, D_, E_, VEC, YT>(a, ep, stream);
     SL_CFG(4, 3, 2, 2, 3)
     SL_CFG(4, 3, 2, 2, 4)
     SL_CFG(2, 3, 2, 2, 3)
     SL_CFG(2, 3, 2, 2, 4)
     SL_CFG(1, 3, 2, 2, 6)
 #undef SL_CFG
-    return launch_cfg<KIND, 1, 1, 2, 2, 8, VEC>(a, ep, stream);
+    return launch_cfg<KIND, 1, 1, 2, 2, 8, VEC, YT>(a, ep, stream);
 }
 
+// The staged kernel writes the block layout only for rows the direct kernel
+// cannot load (k_in % 16 != 0 or a misaligned x): int8 kinds without VEC.
 template <int KIND>
-static sl_status launch_vec(const LinearArgs &a, const GeluArg *ep, TileCfg c, hipStream_t stream, bool vec)
+static sl_status launch_vec(const LinearArgs &a, const GeluArg *ep, TileCfg c, hipStream_t stream, bool vec, bool yt)
 {
-    return vec ? launch_kind<KIND, true>(a, ep, c, stream) : launch_kind<KIND, false>(a, ep, c, stream);
+    if constexpr (EpiOut<KIND>::kBytes == 1) {
+        if (yt) {
+            if (vec) {
+                set_error("internal: aligned rows with a block-layout output go through the direct kernel");
+                return SL_ERR_UNSUPPORTED;
+            }
+            return launch_kind<KIND, false, true>(a, ep, c, stream);
+        }
+    }
+    return vec ? launch_kind<KIND, true, false>(a, ep, c, stream) : launch_kind<KIND, false, false>(a, ep, c, stream);
 }
 
 // Pick the workgroup shape: among shapes that give every CU a workgroup,
@@ -838,8 +884,8 @@ static DirectCfg choose_direct_cfg(int64_t m, const sl_packed_weight *w)
     return best ? *best : *most;
 }
 
-sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int64_t m, float sx, int32_t kind,
-                        float inv_so, void *y, void *stream)
+sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int32_t x_layout, int64_t m, float sx,
+                        int32_t kind, float inv_so, void *y, int32_t y_layout, void *stream)
 {
     int dev = -1;
     HIP_TRY(hipGetDevice(&dev));
@@ -878,19 +924,25 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int64_t m, f
             run_kind = kEpiI8GeluErf;
         }
     }
+    const bool xt = x_layout == SL_LAYOUT_T16X32, yt = y_layout == SL_LAYOUT_T16X32;
+    a.x_cb = (w->k_in + 31) / 32;
+    a.y_cb = (w->n_out + 31) / 32;
     // Token rows go through 32-bit buffer offsets: launch at most
     // kMaxBufferBytes of X at a time (a multiple of every workgroup's tokens).
     const int64_t out_bytes = (kind == SL_EPI_I8 || kind == SL_EPI_I8_GELU) ? 1 : 4;
-    const int64_t chunk = std::max<int64_t>(256, kMaxBufferBytes / std::max<int32_t>(w->k_in, 1) / 256 * 256);
+    const int64_t x_token_bytes = xt ? (int64_t)a.x_cb * 32 : w->k_in;
+    const int64_t chunk = std::max<int64_t>(256, kMaxBufferBytes / std::max<int64_t>(x_token_bytes, 1) / 256 * 256);
     for (int64_t t0 = 0; t0 < m; t0 += chunk) {
-        a.x = x + t0 * w->k_in;
-        a.y = static_cast<char *>(y) + t0 * w->n_out * out_bytes;
+        a.x = x + t0 * x_token_bytes;
+        a.y = static_cast<char *>(y) + (yt ? t0 / 16 * a.y_cb * 512 : t0 * w->n_out * out_bytes);
         a.m = std::min(chunk, m - t0);
-        const bool vec = (w->k_in % 16 == 0) && ((reinterpret_cast<uintptr_t>(a.x) & 15) == 0);
-        // row-major token rows go through the staged kernel; SL_PATH=direct
-        // selects the direct-operand kernel for aligned rows (tests, tuning)
+        const bool vec = xt || ((w->k_in % 16 == 0) && ((reinterpret_cast<uintptr_t>(a.x) & 15) == 0));
+        // Block-layout input, or a block-layout output from aligned rows: the
+        // direct-operand kernel. Row-major input and output: the staged
+        // kernel, unless SL_PATH=direct selects the direct one for aligned
+        // rows (tests, tuning).
         const char *path = getenv("SL_PATH");
-        const bool direct = vec && path && strcmp(path, "direct") == 0;
+        const bool direct = xt || (yt && vec) || (vec && path && strcmp(path, "direct") == 0);
         TileCfg cfg{};
         DirectCfg dcfg{};
         int nt, tm;
@@ -919,15 +971,15 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int64_t m, f
         }
         sl_status st;
         if (direct) {
-            st = launch_direct(a, run_kind == SL_EPI_I8_GELU ? &ga : nullptr, run_kind, dcfg, s);
+            st = launch_direct(a, run_kind == SL_EPI_I8_GELU ? &ga : nullptr, run_kind, dcfg, xt, yt, s);
         } else {
             switch (run_kind) {
-            case SL_EPI_ACC_I32: st = launch_vec<SL_EPI_ACC_I32>(a, nullptr, cfg, s, vec); break;
-            case SL_EPI_F32: st = launch_vec<SL_EPI_F32>(a, nullptr, cfg, s, vec); break;
-            case SL_EPI_F32_GELU: st = launch_vec<SL_EPI_F32_GELU>(a, nullptr, cfg, s, vec); break;
-            case SL_EPI_I8: st = launch_vec<SL_EPI_I8>(a, nullptr, cfg, s, vec); break;
-            case SL_EPI_I8_GELU: st = launch_vec<SL_EPI_I8_GELU>(a, &ga, cfg, s, vec); break;
-            default: st = launch_vec<kEpiI8GeluErf>(a, nullptr, cfg, s, vec); break;
+            case SL_EPI_ACC_I32: st = launch_vec<SL_EPI_ACC_I32>(a, nullptr, cfg, s, vec, yt); break;
+            case SL_EPI_F32: st = launch_vec<SL_EPI_F32>(a, nullptr, cfg, s, vec, yt); break;
+            case SL_EPI_F32_GELU: st = launch_vec<SL_EPI_F32_GELU>(a, nullptr, cfg, s, vec, yt); break;
+            case SL_EPI_I8: st = launch_vec<SL_EPI_I8>(a, nullptr, cfg, s, vec, yt); break;
+            case SL_EPI_I8_GELU: st = launch_vec<SL_EPI_I8_GELU>(a, &ga, cfg, s, vec, yt); break;
+            default: st = launch_vec<kEpiI8GeluErf>(a, nullptr, cfg, s, vec, yt); break;
             }
         }
         if (st != SL_OK) return st;
@@ -952,6 +1004,24 @@ sl_status launch_quantize(const float *x, int64_t n, float inv_scale, int8_t *q,
                            inv_scale, q + n16 * 16);
         HIP_TRY(hipGetLastError());
     }
+    return SL_OK;
+}
+
+sl_status launch_quantize_t16x32(const float *x, int64_t rows, int32_t cols, float inv_scale, int8_t *q,
+                                 void *stream)
+{
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int32_t cblocks = (cols + 31) / 32;
+    const int64_t n_pieces = (rows + 15) / 16 * cblocks * 32;
+    const int64_t blocks = std::min<int64_t>((n_pieces + 255) / 256, 256 * 16);
+    const bool vec = cols % 4 == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0;
+    if (vec)
+        hipLaunchKernelGGL(quantize_t16x32_kernel<true>, dim3((uint32_t)blocks), dim3(256), 0, s, x, rows, cols,
+                           cblocks, n_pieces, inv_scale, q);
+    else
+        hipLaunchKernelGGL(quantize_t16x32_kernel<false>, dim3((uint32_t)blocks), dim3(256), 0, s, x, rows, cols,
+                           cblocks, n_pieces, inv_scale, q);
+    HIP_TRY(hipGetLastError());
     return SL_OK;
 }
 

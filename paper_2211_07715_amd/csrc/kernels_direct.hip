@@ -31,8 +31,9 @@ namespace sl {
 
 // Workgroup shape: WM compute waves along the tokens, each with ST 16-token
 // subtiles x all NT 16-channel tiles; as many copy waves; D windows in flight.
-// One window's buffer: NT main operands, then up to NT packed overflow
-// operands; each region is padded to whole 64-lane copies per copy wave.
+// One window's buffer: NT main operands, then NT overflow operand slots (one
+// per tile, zeros where the tile has none); each region is padded to whole
+// 64-lane copies per copy wave.
 template <int ST, int NT, int WM, int D>
 struct DShape {
     static constexpr int NW = WM;
@@ -41,15 +42,16 @@ struct DShape {
     static constexpr int TM = 16 * ST * WM;                      // tokens per work item
     static constexpr int CA = (NT * kOpPieces + NTH - 1) / NTH;  // copies per copy wave per region
     static constexpr int AB = CA * NTH * 16;
-    static constexpr int COPIES = 2 * CA + 1;  // per copy wave per window: main, mask, overflow
+    static constexpr int COPIES = 2 * CA;  // per copy wave per window: main, overflow
     static constexpr int BUF = 2 * AB;
     static constexpr int LDS = D * BUF;
     static constexpr int VEC = 2 * NT * kTileN * 4;  // per compute wave: weight scales, then biases
-    static constexpr int MASKS = D * NW * 4;         // per ring buffer and copy wave: the overflow mask
     static_assert(NT <= 32, "an overflow mask has 32 bits");
 };
 
-template <int KIND, int ST, int NT, int WM, int D>
+// XT: x in SL_LAYOUT_T16X32 (else row-major, 16-byte aligned rows); YT: y in
+// SL_LAYOUT_T16X32 (int8 kinds).
+template <int KIND, int ST, int NT, int WM, int D, bool XT, bool YT>
 __device__ __forceinline__ void direct_body(const LinearArgs &a, const GeluArg *ep)
 {
     using S = DShape<ST, NT, WM, D>;
@@ -73,11 +75,9 @@ __device__ __forceinline__ void direct_body(const LinearArgs &a, const GeluArg *
         return p >= a.n_win ? p - a.n_win : p;
     };
 
-    // LDS: the ring, the GELU table, the compute waves' scales and biases,
-    // the overflow masks
+    // LDS: the ring, the GELU table, the compute waves' scales and biases
     GeluCell *tab = reinterpret_cast<GeluCell *>(smem + S::LDS);
     constexpr int kTabBytes = KIND == SL_EPI_I8_GELU ? kGeluLds : 0;
-    uint32_t *omask = reinterpret_cast<uint32_t *>(smem + S::LDS + kTabBytes + S::NW * S::VEC);
     float hinv = 0.0f, eoff = 0.0f, cmax = 0.0f;
     if constexpr (KIND == SL_EPI_I8_GELU) {
         for (int u = copier ? ep->nc : tid; u < ep->nc; u += S::NTH) tab[u] = ep->cell[u];
@@ -107,10 +107,8 @@ __device__ __forceinline__ void direct_body(const LinearArgs &a, const GeluArg *
             __builtin_amdgcn_make_buffer_rsrc((void *)a.main, 0, (int)a.main_bytes, kRsrcWord3);
         const __amdgpu_buffer_rsrc_t orc =
             __builtin_amdgcn_make_buffer_rsrc((void *)a.ovf, 0, (int)a.ovf_bytes, kRsrcWord3);
-        const __amdgpu_buffer_rsrc_t omr =
-            __builtin_amdgcn_make_buffer_rsrc((void *)a.om, 0, a.n_win * a.n_cgroups * 8, kRsrcWord3);
         const uint32_t wstride = (uint32_t)a.n_tiles * kOpBytes;  // main image bytes per window
-        // this lane's piece of each main-operand copy
+        // this lane's piece (tile, 16-byte piece) of each operand-region copy
         int32_t atile[S::CA], apiece16[S::CA];
 #pragma unroll
         for (int i = 0; i < S::CA; ++i) {
@@ -144,42 +142,31 @@ __device__ __forceinline__ void direct_body(const LinearArgs &a, const GeluArg *
         item_offsets();
 
         // Copy k (0 <= k < COPIES) of the cursor's element (physical window
-        // w) into ring buffer bi: main operands, the overflow mask (one lane,
-        // 4 bytes), then the packed overflow operands (o: the element's
-        // overflow entry; the item's overflow operands of a window are
-        // consecutive in the image, from index o.y on).
-        constexpr int KM = S::CA;
+        // w) into ring buffer bi: main operands, then the overflow operands
+        // into the slot of their tile (o: the element's overflow entry: mask
+        // of the item's tiles that have one, index of the first; zeros for
+        // the others).
         auto copy = [&](int k, int w, int bi, uint2 o) {
             int8_t *b = smem + bi * S::BUF;
-            if (k < KM) {
+            if (k < S::CA) {
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(mr, (lds_void *)(b + (k * S::NW + pw) * 1024), 16, aoff[k],
                                                          (uint32_t)w * wstride, 0, 0);
-            } else if (k == KM) {
-                if (lane == 0)
-                    __builtin_amdgcn_raw_ptr_buffer_load_lds(omr, (lds_void *)(omask + bi * S::NW + pw), 4,
-                                                             (uint32_t)(w * a.n_cgroups + ic.cg) * 8u, 0, 0, 0);
             } else {
-                const int i = k - KM - 1;
-                const int q0 = (i * S::NW + pw) * 64;  // first packed piece of this copy
-                const int npieces = __builtin_popcount(o.x) * kOpPieces;
-                lds_void *dst = (lds_void *)(b + S::AB + (i * S::NW + pw) * 1024);
-                if (q0 < npieces) {
-                    const int q = q0 + lane;
-                    const uint32_t off = q < npieces ? o.y * (uint32_t)kOpBytes + (uint32_t)q * 16u : kOob;
-                    __builtin_amdgcn_raw_ptr_buffer_load_lds(orc, dst, 16, off, 0, 0, 0);
-                } else if (lane == 0) {
-                    // nothing to copy: one lane keeps the count (16 zero bytes
-                    // past the packed operands)
-                    __builtin_amdgcn_raw_ptr_buffer_load_lds(orc, dst, 16, kOob, 0, 0, 0);
-                }
+                const int i = k - S::CA;
+                const uint32_t t = (uint32_t)atile[i];
+                const bool has = t < 32u && ((o.x >> t) & 1u);
+                const uint32_t rank = __builtin_popcount(o.x & ((1u << (t & 31u)) - 1u));
+                const uint32_t off = has ? (o.y + rank) * (uint32_t)kOpBytes + (uint32_t)apiece16[i] : kOob;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(orc, (lds_void *)(b + S::AB + (i * S::NW + pw) * 1024), 16,
+                                                         off, 0, 0, 0);
             }
         };
 
         // Prologue: the overflow entries of elements 0..D-1 start loading; the
-        // main operands and masks of those elements are copied; a bare
-        // barrier (A) publishes the epilogue table the compute waves filled;
-        // the overflow operands follow; once element 0 has landed a second
-        // barrier (B) publishes it.
+        // main operands of those elements are copied; a bare barrier (A)
+        // publishes the epilogue table the compute waves filled; the overflow
+        // operands follow; once element 0 has landed a second barrier (B)
+        // publishes it.
         uint2 o[D];
         {
             const ItemIter ic0 = ic;
@@ -201,7 +188,7 @@ __device__ __forceinline__ void direct_body(const LinearArgs &a, const GeluArg *
         for (int d = 0; d < D; ++d) {
             wp[d] = cur_w();
 #pragma unroll
-            for (int k = 0; k <= KM; ++k) copy(k, wp[d], d, make_uint2(0u, 0u));
+            for (int k = 0; k < S::CA; ++k) copy(k, wp[d], d, make_uint2(0u, 0u));
             advance();
         }
         __builtin_amdgcn_s_barrier();  // (A)
@@ -209,7 +196,7 @@ __device__ __forceinline__ void direct_body(const LinearArgs &a, const GeluArg *
 #pragma unroll
         for (int d = 0; d < D; ++d) {
 #pragma unroll
-            for (int k = KM + 1; k < S::COPIES; ++k) copy(k, wp[d], d, o[d]);
+            for (int k = S::CA; k < S::COPIES; ++k) copy(k, wp[d], d, o[d]);
         }
         uint2 onx = om_at(ic, cur_w());  // entry of element D
         wait_vmcnt_le<(D - 1) * S::CA>();  // element 0 landed
@@ -250,23 +237,32 @@ __device__ __forceinline__ void direct_body(const LinearArgs &a, const GeluArg *
     // this lane's index word: block-row (lane%16)/4, lane group lane/16
     const int iword = ((lane & 15) >> 2) * 4 + (lane >> 4);
 
-    // Token rows: lane l of subtile s loads bytes 32*(l/16) .. +31 of its
-    // window of token row (l % 16) -- the B operand layout. Rows past m read
-    // zeros (out-of-range offsets); a ragged last window reads the next row's
-    // first bytes (or zeros past the buffer), which meet zero weights.
+    // Token rows: lane l of subtile s loads features 32*(l/16) .. +31 of its
+    // window for token (l % 16) -- the B operand layout. Row-major: 32 bytes
+    // of the token's row; block layout: 32 bytes of the token's row in block
+    // 4w + l/16, so each group of 4 lanes reads one cache line. Tokens past m
+    // read zeros (out-of-range offsets) or a padding token of the last block;
+    // a ragged last window reads bytes past the row (or zeros past the
+    // buffer), which meet zero weights.
+    const int64_t xbytes = XT ? (a.m + 15) / 16 * a.x_cb * 512 : a.m * a.k;
     const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
-        (void *)a.x, 0, (int)min<int64_t>(a.m * a.k, kMaxBufferBytes), kRsrcWord3);
+        (void *)a.x, 0, (int)min<int64_t>(xbytes, kMaxBufferBytes), kRsrcWord3);
     auto row_offsets = [&](const ItemIter &it, uint32_t (&ro)[ST]) {
 #pragma unroll
         for (int s = 0; s < ST; ++s) {
             const int64_t r = (int64_t)it.mt * S::TM + wm * ST * 16 + s * 16 + (lane & 15);
-            ro[s] = r < a.m ? (uint32_t)(r * a.k) + 32u * (uint32_t)(lane >> 4) : kOob;
+            if constexpr (XT)
+                ro[s] = r < (a.m + 15) / 16 * 16 ? (uint32_t)((r >> 4) * a.x_cb * 512) + 512u * (uint32_t)(lane >> 4) +
+                                                       32u * (uint32_t)(lane & 15)
+                                                 : kOob;
+            else
+                ro[s] = r < a.m ? (uint32_t)(r * a.k) + 32u * (uint32_t)(lane >> 4) : kOob;
         }
     };
     auto load_rows = [&](i32x8 (&bv)[ST], const uint32_t (&ro)[ST], int w) {
 #pragma unroll
         for (int s = 0; s < ST; ++s) {
-            const uint32_t off = ro[s] + (uint32_t)w * kWin;
+            const uint32_t off = ro[s] + (uint32_t)w * (XT ? 4 * 512 : kWin);
             const i32x4 lo = __builtin_bit_cast(i32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0));
             const i32x4 hi = __builtin_bit_cast(i32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, off + 16u, 0, 0));
             bv[s] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
@@ -274,28 +270,28 @@ __device__ __forceinline__ void direct_body(const LinearArgs &a, const GeluArg *
     };
 
     // Weight operands of one element in registers: main and overflow A
-    // operands with their index words. Two sets alternate (steps e, e+1).
+    // operands of every tile with their index words (an absent overflow
+    // operand is zeros: its products are zero). Two sets alternate (steps e,
+    // e+1), for the token rows too: element e+1's rows load at the start of
+    // step e, into the set whose matrix instructions (step e-1's) have been
+    // issued before the barrier, so the loads do not wait for them.
     struct Ops {
         i32x4 av[NT], ao[NT];
         int ix[NT], io[NT];
     };
     Ops ops[2];
-    i32x8 bv[2][ST];  // token rows of elements e (set e & 1) and e+1
-    auto read_main = [&](Ops &r, const int8_t *b) {
+    i32x8 bv[2][ST];
+    auto read_ops = [&](Ops &r, const int8_t *b) {
 #pragma unroll
         for (int c = 0; c < NT; ++c) {
             const int8_t *op = b + c * kOpBytes;
             r.av[c] = *reinterpret_cast<const i32x4 *>(op + lane * 16);
             r.ix[c] = *reinterpret_cast<const int *>(op + 1024 + iword * 4);
+            const int8_t *oo = b + S::AB + c * kOpBytes;
+            r.ao[c] = *reinterpret_cast<const i32x4 *>(oo + lane * 16);
+            r.io[c] = *reinterpret_cast<const int *>(oo + 1024 + iword * 4);
         }
     };
-    // overflow operand of tile c, packed at rank j
-    auto read_ovf = [&](Ops &r, const int8_t *b, int c, int j) {
-        const int8_t *oo = b + S::AB + j * kOpBytes;
-        r.ao[c] = *reinterpret_cast<const i32x4 *>(oo + lane * 16);
-        r.io[c] = *reinterpret_cast<const int *>(oo + 1024 + iword * 4);
-    };
-    auto read_mask = [&](int b) { return (uint32_t)__builtin_amdgcn_readfirstlane((int)omask[b * S::NW]); };
 
     // the item's weight scales and biases, one copy each into this wave's
     // LDS area (NT*4 lanes of 16 bytes); the epilogue waits for them
@@ -343,20 +339,28 @@ __device__ __forceinline__ void direct_body(const LinearArgs &a, const GeluArg *
                 for (int r = 0; r < 4; ++r) s[r] = bb4[r] = 0.0f;
             }
         };
-        if (t0 + ST * 16 <= a.m && (tile0 + NT) * kTileN <= a.n) {
+        // in the block layout the padding tokens of the last block may be
+        // written too
+        const int64_t mlim = YT ? (a.m + 15) / 16 * 16 : a.m;
+        if (t0 + ST * 16 <= mlim && (tile0 + NT) * kTileN <= a.n) {
             // whole tile: a uniform base and a lane offset, no bounds checks
             using T = typename EpiOut<KIND>::T;
             constexpr int EB = EpiOut<KIND>::kBytes;
-            int8_t *base = static_cast<int8_t *>(a.y) + (t0 * a.n + (int64_t)tile0 * kTileN) * EB;
-            const uint32_t lo = (uint32_t)(((lane & 15) * a.n + 4 * (lane >> 4)) * EB);
+            int8_t *const y8 = static_cast<int8_t *>(a.y);
+            const uint32_t lo = YT ? (uint32_t)(32 * (lane & 15) + 4 * (lane >> 4))
+                                   : (uint32_t)(((lane & 15) * a.n + 4 * (lane >> 4)) * EB);
 #pragma unroll
             for (int c = 0; c < NT; ++c) {
                 float s[4], bb4[4];
                 scales(c, s, bb4);
 #pragma unroll
-                for (int st = 0; st < ST; ++st)
-                    *reinterpret_cast<T *>(base + lo + ((int64_t)st * 16 * a.n + c * kTileN) * EB) =
+                for (int st = 0; st < ST; ++st) {
+                    const int32_t ch = (tile0 + c) * kTileN;
+                    const int64_t uo = YT ? t16x32_offset(t0 + st * 16, ch, a.y_cb)
+                                          : ((t0 + st * 16) * a.n + ch) * EB;
+                    *reinterpret_cast<T *>(y8 + uo + lo) =
                         epilogue_value<KIND>(a, acc[c][st], s, bb4, tab, hinv, eoff, cmax);
+                }
             }
         } else {
 #pragma unroll
@@ -369,19 +373,20 @@ __device__ __forceinline__ void direct_body(const LinearArgs &a, const GeluArg *
                 scales(c, s, bb4);
 #pragma unroll
                 for (int st = 0; st < ST; ++st)
-                    epilogue_store<KIND>(a, acc[c][st], t0 + st * 16 + (lane & 15), ch0, s, bb4, tab, hinv, eoff,
-                                         cmax);
+                    epilogue_store<KIND, YT>(a, acc[c][st], t0 + st * 16 + (lane & 15), ch0, s, bb4, tab, hinv,
+                                             eoff, cmax);
             }
         }
     };
 
-    // element cursors: the token rows of element e+2 are loaded in step e
-    // (item ib, window wb); sl is element e's ring buffer
+    // element cursor of the token-row loads (element e+1 in step e: item ib,
+    // window wb); sl: element e's ring buffer
     ItemIter ib = first;
     int kb = 0, wb = 0;
     uint32_t rob[ST];
     row_offsets(ib, rob);
-    auto advance_b = [&]() {
+    auto load_next_rows = [&](i32x8 (&dst)[ST]) {
+        load_rows(dst, rob, phys(ib, kb < n_my ? wb : a.n_win - 1));
         if (++wb == a.n_win) {
             wb = 0;
             if (++kb < n_my) {
@@ -390,97 +395,73 @@ __device__ __forceinline__ void direct_body(const LinearArgs &a, const GeluArg *
             }
         }
     };
-    auto load_next_rows = [&](i32x8 (&dst)[ST]) {
-        load_rows(dst, rob, phys(ib, kb < n_my ? wb : a.n_win - 1));
-        advance_b();
-    };
     int sl = 0;
-    int64_t e = 0;
-    uint32_t mask_w;  // overflow mask of element e
-    auto step = [&](auto pr) {
-        constexpr int PR = decltype(pr)::value;
-        Ops &cur = ops[PR];
-        Ops &nxt = ops[PR ^ 1];
+    // step of element e with its weight operands and token rows in set PA
+    // (e % 2)
+    auto step = [&](auto pa) {
+        constexpr int PA = decltype(pa)::value;
+        Ops &cur = ops[PA];
+        Ops &nxt = ops[PA ^ 1];
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
-        const int sl1 = sl + 1 == D ? 0 : sl + 1;
-        const int8_t *nb = smem + sl1 * S::BUF;
-        // Main part: element e+1's main operand reads and element e's main
-        // matrix instructions, one after the other. Products of tiles past
-        // the item's last tile land in accumulators that are never stored.
-        read_main(nxt, nb);
+        load_next_rows(bv[PA ^ 1]);  // element e+1's token rows
+        sl = sl + 1 == D ? 0 : sl + 1;
+        // element e+1's operand reads, one before each matrix instruction of
+        // element e, so that a read waiting for room in the LDS queue does not
+        // leave the matrix core idle. (The last step reads a stale buffer:
+        // harmless.) Products of tiles past the item's last tile land in
+        // accumulators that are never stored.
+        read_ops(nxt, smem + sl * S::BUF);
+        // (all main products first, then the overflow ones: an instruction
+        // never waits for the result of the one just before it)
 #pragma unroll
         for (int c = 0; c < NT; ++c)
 #pragma unroll
             for (int s = 0; s < ST; ++s)
                 acc[c][s] =
-                    __builtin_amdgcn_smfmac_i32_16x16x128_i8(cur.av[c], bv[PR][s], acc[c][s], cur.ix[c], 0, 0);
+                    __builtin_amdgcn_smfmac_i32_16x16x128_i8(cur.av[c], bv[PA][s], acc[c][s], cur.ix[c], 0, 0);
 #pragma unroll
-        for (int v = 0; v < NT * ST; ++v) {
+        for (int c = 0; c < NT; ++c)
+#pragma unroll
+            for (int s = 0; s < ST; ++s)
+                acc[c][s] =
+                    __builtin_amdgcn_smfmac_i32_16x16x128_i8(cur.ao[c], bv[PA][s], acc[c][s], cur.io[c], 0, 0);
+#pragma unroll
+        for (int v = 0; v < 4 * NT; ++v) {
             __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one matrix instruction
         }
-        __builtin_amdgcn_sched_group_barrier(0x100, 2 * NT, 0);  // the remaining reads
-        // element e+1's overflow mask, read once the main matrix instructions
-        // are queued (its latency hides behind them)
-        __builtin_amdgcn_sched_barrier(0);
-        const uint32_t mask_n = read_mask(sl1);
-        // overflow part, per tile (packed operands: rank = set bits below)
-#pragma unroll
-        for (int c = 0; c < NT; ++c) {
-            if (e + 1 < steps && ((mask_n >> c) & 1u))
-                read_ovf(nxt, nb, c, __builtin_popcount(mask_n & ((1u << c) - 1u)));
-            if ((mask_w >> c) & 1u) {
-#pragma unroll
-                for (int s = 0; s < ST; ++s)
-                    acc[c][s] =
-                        __builtin_amdgcn_smfmac_i32_16x16x128_i8(cur.ao[c], bv[PR][s], acc[c][s], cur.io[c], 0, 0);
-            }
-        }
-        // element e's token rows are consumed: load element e+2's into the set
-        load_next_rows(bv[PR]);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2 * NT * ST, 0);  // the remaining matrix instructions
         // element e+1's buffer is refilled after the next barrier: its reads
         // must be done by then
         wait_lgkm0();
-        mask_w = mask_n;
-        sl = sl1;
-        ++e;
     };
-    using P0 = std::integral_constant<int, 0>;
-    using P1 = std::integral_constant<int, 1>;
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
 
     ItemIter it = first;
     clear_acc();
     fetch_vec(it);
     load_next_rows(bv[0]);
-    load_next_rows(bv[1]);
     __builtin_amdgcn_s_barrier();  // (B): element 0 has landed
     asm volatile("" ::: "memory");
-    mask_w = read_mask(0);
-    read_main(ops[0], smem);
-#pragma unroll
-    for (int c = 0; c < NT; ++c)
-        if ((mask_w >> c) & 1u) read_ovf(ops[0], smem, c, __builtin_popcount(mask_w & ((1u << c) - 1u)));
+    read_ops(ops[0], smem);
     wait_lgkm0();  // element 0's buffer is refilled after the next barrier
-    // Each item starts with its first element's operands in set 0; after an
-    // odd number of windows they are moved there from set 1.
+    // Each item starts with its first element in set 0; after an odd number
+    // of windows the next element's operands are moved there from set 1.
     for (int k = 0; k < n_my; ++k) {
         int w = 0;
         for (; w + 2 <= a.n_win; w += 2) {
-            step(P0{});
-            step(P1{});
+            step(I0{});
+            step(I1{});
         }
+        if (w < a.n_win) step(I0{});
+        epilogue(it);  // (waits for every load: the moves below read loaded registers)
         if (w < a.n_win) {
-            step(P0{});
             ops[0] = ops[1];
 #pragma unroll
-            for (int s = 0; s < ST; ++s) {
-                const i32x8 t = bv[0][s];
-                bv[0][s] = bv[1][s];
-                bv[1][s] = t;
-            }
+            for (int s = 0; s < ST; ++s) bv[0][s] = bv[1][s];
         }
-        epilogue(it);
         if (k + 1 < n_my) {
             clear_acc();
             it.next();
@@ -490,49 +471,50 @@ __device__ __forceinline__ void direct_body(const LinearArgs &a, const GeluArg *
     }
 }
 
-template <int KIND, int ST, int NT, int WM, int D>
+template <int KIND, int ST, int NT, int WM, int D, bool XT, bool YT>
 __global__ __launch_bounds__(128 * WM) void sparse_linear_direct_kernel(LinearArgs a)
 {
-    direct_body<KIND, ST, NT, WM, D>(a, nullptr);
+    direct_body<KIND, ST, NT, WM, D, XT, YT>(a, nullptr);
 }
 
-template <int ST, int NT, int WM, int D>
+template <int ST, int NT, int WM, int D, bool XT, bool YT>
 __global__ __launch_bounds__(128 * WM) void sparse_linear_direct_gelu_kernel(LinearArgs a, GeluArg ep)
 {
-    direct_body<SL_EPI_I8_GELU, ST, NT, WM, D>(a, &ep);
+    direct_body<SL_EPI_I8_GELU, ST, NT, WM, D, XT, YT>(a, &ep);
 }
 
-template <int KIND, int ST, int NT, int WM, int D>
+template <int KIND, int ST, int NT, int WM, int D, bool XT, bool YT>
 static sl_status launch_direct_cfg(const LinearArgs &a, const GeluArg *ep, hipStream_t stream)
 {
     using S = DShape<ST, NT, WM, D>;
     const void *fn;
     if constexpr (KIND == SL_EPI_I8_GELU)
-        fn = reinterpret_cast<const void *>(&sparse_linear_direct_gelu_kernel<ST, NT, WM, D>);
+        fn = reinterpret_cast<const void *>(&sparse_linear_direct_gelu_kernel<ST, NT, WM, D, XT, YT>);
     else
-        fn = reinterpret_cast<const void *>(&sparse_linear_direct_kernel<KIND, ST, NT, WM, D>);
-    const size_t lds = (size_t)S::LDS + S::NW * S::VEC + S::MASKS + (KIND == SL_EPI_I8_GELU ? kGeluLds : 0);
-    static_assert(S::LDS + S::NW * S::VEC + S::MASKS + kGeluLds <= kLdsMax, "workgroup shape exceeds LDS");
+        fn = reinterpret_cast<const void *>(&sparse_linear_direct_kernel<KIND, ST, NT, WM, D, XT, YT>);
+    const size_t lds = (size_t)S::LDS + S::NW * S::VEC + (KIND == SL_EPI_I8_GELU ? kGeluLds : 0);
+    static_assert(S::LDS + S::NW * S::VEC + kGeluLds <= kLdsMax, "workgroup shape exceeds LDS");
     static int resident[kMaxDevices] = {};  // per kernel instance and device
     int grid = 0;
     const sl_status st = persistent_grid(fn, S::NTHG, lds, resident, &grid);
     if (st != SL_OK) return st;
     const int64_t nwg = std::min<int64_t>(a.n_items, grid);
     if constexpr (KIND == SL_EPI_I8_GELU)
-        hipLaunchKernelGGL((sparse_linear_direct_gelu_kernel<ST, NT, WM, D>), dim3((uint32_t)nwg), dim3(S::NTHG), lds,
-                           stream, a, *ep);
+        hipLaunchKernelGGL((sparse_linear_direct_gelu_kernel<ST, NT, WM, D, XT, YT>), dim3((uint32_t)nwg),
+                           dim3(S::NTHG), lds, stream, a, *ep);
     else
-        hipLaunchKernelGGL((sparse_linear_direct_kernel<KIND, ST, NT, WM, D>), dim3((uint32_t)nwg), dim3(S::NTHG),
-                           lds, stream, a);
+        hipLaunchKernelGGL((sparse_linear_direct_kernel<KIND, ST, NT, WM, D, XT, YT>), dim3((uint32_t)nwg),
+                           dim3(S::NTHG), lds, stream, a);
     HIP_TRY(hipGetLastError());
     return SL_OK;
 }
 
-template <int KIND>
+template <int KIND, bool XT, bool YT>
 static sl_status launch_direct_kind(const LinearArgs &a, const GeluArg *ep, DirectCfg c, hipStream_t stream)
 {
-#define SL_DCFG(A_, B_, C_, D_) \
-    if (c.st == A_ && c.nt == B_ && c.wm == C_ && c.d == D_) return launch_direct_cfg<KIND, A_, B_, C_, D_>(a, ep, stream);
+#define SL_DCFG(A_, B_, C_, D_)                                \
+    if (c.st == A_ && c.nt == B_ && c.wm == C_ && c.d == D_) \
+        return launch_direct_cfg<KIND, A_, B_, C_, D_, XT, YT>(a, ep, stream);
     SL_DCFG(2, 6, 4, 4)
     SL_DCFG(1, 6, 4, 6)
     SL_DCFG(1, 2, 4, 8)
@@ -547,15 +529,31 @@ const DirectCfg kDirectCfgs[kNumDirectCfgs] = {
     {1, 2, 4, 8},  //  64 tokens x 32 channels (few work items)
 };
 
-sl_status launch_direct(const LinearArgs &a, const GeluArg *ep, int32_t run_kind, DirectCfg c, hipStream_t stream)
+template <int KIND, bool XT>
+static sl_status launch_direct_y(const LinearArgs &a, const GeluArg *ep, DirectCfg c, bool yt, hipStream_t stream)
+{
+    if constexpr (EpiOut<KIND>::kBytes == 1)
+        if (yt) return launch_direct_kind<KIND, XT, true>(a, ep, c, stream);
+    return launch_direct_kind<KIND, XT, false>(a, ep, c, stream);
+}
+
+template <int KIND>
+static sl_status launch_direct_x(const LinearArgs &a, const GeluArg *ep, DirectCfg c, bool xt, bool yt,
+                                 hipStream_t stream)
+{
+    return xt ? launch_direct_y<KIND, true>(a, ep, c, yt, stream) : launch_direct_y<KIND, false>(a, ep, c, yt, stream);
+}
+
+sl_status launch_direct(const LinearArgs &a, const GeluArg *ep, int32_t run_kind, DirectCfg c, bool xt, bool yt,
+                        hipStream_t stream)
 {
     switch (run_kind) {
-    case SL_EPI_ACC_I32: return launch_direct_kind<SL_EPI_ACC_I32>(a, nullptr, c, stream);
-    case SL_EPI_F32: return launch_direct_kind<SL_EPI_F32>(a, nullptr, c, stream);
-    case SL_EPI_F32_GELU: return launch_direct_kind<SL_EPI_F32_GELU>(a, nullptr, c, stream);
-    case SL_EPI_I8: return launch_direct_kind<SL_EPI_I8>(a, nullptr, c, stream);
-    case SL_EPI_I8_GELU: return launch_direct_kind<SL_EPI_I8_GELU>(a, ep, c, stream);
-    default: return launch_direct_kind<kEpiI8GeluErf>(a, nullptr, c, stream);
+    case SL_EPI_ACC_I32: return launch_direct_x<SL_EPI_ACC_I32>(a, nullptr, c, xt, yt, stream);
+    case SL_EPI_F32: return launch_direct_x<SL_EPI_F32>(a, nullptr, c, xt, yt, stream);
+    case SL_EPI_F32_GELU: return launch_direct_x<SL_EPI_F32_GELU>(a, nullptr, c, xt, yt, stream);
+    case SL_EPI_I8: return launch_direct_x<SL_EPI_I8>(a, nullptr, c, xt, yt, stream);
+    case SL_EPI_I8_GELU: return launch_direct_x<SL_EPI_I8_GELU>(a, ep, c, xt, yt, stream);
+    default: return launch_direct_x<kEpiI8GeluErf>(a, nullptr, c, xt, yt, stream);
     }
 }
 

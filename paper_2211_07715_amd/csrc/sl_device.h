@@ -55,7 +55,16 @@ struct LinearArgs {
     int32_t n_win;
     int32_t n_cgroups;  // channel groups of NT tiles
     int64_t n_items;    // work items: token tiles x channel groups
+    int32_t x_cb;       // 32-feature column blocks of x (SL_LAYOUT_T16X32 input)
+    int32_t y_cb;       // 32-channel column blocks of y (SL_LAYOUT_T16X32 output)
 };
+
+// Byte offset of element (t, c) of an int8 tensor in SL_LAYOUT_T16X32 with
+// cb column blocks: 512-byte blocks of 16 tokens x 32 features.
+__device__ __forceinline__ int64_t t16x32_offset(int64_t t, int32_t c, int32_t cb)
+{
+    return ((t >> 4) * cb + (c >> 5)) * 512 + (t & 15) * 32 + (c & 31);
+}
 
 // internal kind: GELU + requantisation evaluated with erf (no usable table)
 constexpr int kEpiI8GeluErf = 5;
@@ -165,16 +174,18 @@ __device__ __forceinline__ typename EpiOut<KIND>::T epilogue_value(const LinearA
 }
 
 // Epilogue and store of one accumulator group at token tok, channels
-// ch0..ch0+3 (nothing past the last token).
-template <int KIND>
+// ch0..ch0+3 (nothing past the last token). YT: y in SL_LAYOUT_T16X32 (int8
+// kinds only), else row-major.
+template <int KIND, bool YT = false>
 __device__ __forceinline__ void epilogue_store(const LinearArgs &a, const i32x4 acc, int64_t tok, int32_t ch0,
                                                const float s[4], const float b[4], const GeluCell *tab,
                                                float hinv, float off, float cmax)
 {
     if (tok >= a.m) return;
     using T = typename EpiOut<KIND>::T;
-    *reinterpret_cast<T *>(static_cast<int8_t *>(a.y) + (tok * a.n + ch0) * EpiOut<KIND>::kBytes) =
-        epilogue_value<KIND>(a, acc, s, b, tab, hinv, off, cmax);
+    static_assert(!YT || EpiOut<KIND>::kBytes == 1, "the block layout holds int8 outputs");
+    const int64_t o = YT ? t16x32_offset(tok, ch0, a.y_cb) : (tok * a.n + ch0) * EpiOut<KIND>::kBytes;
+    *reinterpret_cast<T *>(static_cast<int8_t *>(a.y) + o) = epilogue_value<KIND>(a, acc, s, b, tab, hinv, off, cmax);
 }
 
 typedef __attribute__((address_space(3))) void lds_void;
@@ -255,8 +266,10 @@ struct DirectCfg {
 };
 constexpr int kNumDirectCfgs = 3;
 extern const DirectCfg kDirectCfgs[kNumDirectCfgs];
-// run_kind: an SL_EPI_* kind or kEpiI8GeluErf; ep: the GELU table for SL_EPI_I8_GELU
-sl_status launch_direct(const LinearArgs &a, const GeluArg *ep, int32_t run_kind, DirectCfg c, hipStream_t stream);
+// run_kind: an SL_EPI_* kind or kEpiI8GeluErf; ep: the GELU table for
+// SL_EPI_I8_GELU; xt / yt: x / y in SL_LAYOUT_T16X32 (yt for int8 kinds)
+sl_status launch_direct(const LinearArgs &a, const GeluArg *ep, int32_t run_kind, DirectCfg c, bool xt, bool yt,
+                        hipStream_t stream);
 
 // Persistent grid size of a kernel on the current device: the workgroups of
 // `threads` threads and `lds` bytes of dynamic LDS resident at once. On first

@@ -120,8 +120,10 @@ sl_status decode_tile_image(const sl_packed_weight *w, int8_t *dense);
 sl_status upload_image(sl_packed_weight *w);
 void release_image(sl_packed_weight *w);
 sl_status check_device_arch(int *device);
-sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int64_t m, float sx, int32_t kind,
-                        float inv_so, void *y, void *stream);
+sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int32_t x_layout, int64_t m, float sx,
+                        int32_t kind, float inv_so, void *y, int32_t y_layout, void *stream);
 sl_status launch_quantize(const float *x, int64_t n, float inv_scale, int8_t *q, void *stream);
+sl_status launch_quantize_t16x32(const float *x, int64_t rows, int32_t cols, float inv_scale, int8_t *q,
+                                 void *stream);
 
 }  // namespace sl

@@ -31,7 +31,7 @@ def test_library_exports_every_declared_symbol():
     assert declared == set(sl.EXPORTS), declared ^ set(sl.EXPORTS)
     for name in declared:
         assert hasattr(lib, name), name
-    assert lib.sl_abi_version() == 1
+    assert lib.sl_abi_version() == 2
     assert lib.sl_status_string(-2) == b"SL_ERR_SHAPE"
 
 
@@ -182,3 +182,45 @@ def test_quantize_act_argument_checks_without_gpu():
     assert lib.quantize_act(None, 4, 0.0, None, None) == -1
     assert lib.quantize_act(None, 4, float("nan"), None, None) == -1
     assert lib.quantize_act(None, 4, 1.0, None, None) == -1     # NULL buffers
+
+
+def test_run_layout_argument_checks_without_gpu():
+    lib = sl.load()
+    w = np.ones((8, 8), np.int8)
+    pw = sl.PackedWeight.pack(w, np.ones(8, np.float32), host_only=True)
+    p = ctypes.c_void_p(16)
+    assert lib.sparse_linear_run_layout(None, p, 0, 4, 1.0, 1, 1.0, p, 0, None) == -1
+    assert lib.sparse_linear_run_layout(pw.handle, p, 1, 4, 1.0, 3, 1.0, p, 1, None) == -6
+    pw.free()
+
+
+def test_quantize_act_layout_argument_checks_without_gpu():
+    lib = sl.load()
+    assert lib.quantize_act_layout(None, 0, 8, 1.0, None, 1, None) == 0      # empty: no-op
+    assert lib.quantize_act_layout(None, 4, 0, 1.0, None, 1, None) == 0
+    assert lib.quantize_act_layout(None, -1, 8, 1.0, None, 1, None) == -2
+    assert lib.quantize_act_layout(None, 4, -8, 1.0, None, 1, None) == -2
+    assert lib.quantize_act_layout(None, 4, 8, 1.0, None, 7, None) == -1     # unknown layout
+    assert lib.quantize_act_layout(None, 4, 8, 0.0, None, 1, None) == -1
+    assert lib.quantize_act_layout(None, 4, 8, 1.0, None, 1, None) == -1     # NULL pointers
+    # 16-byte alignment of the block-layout output
+    assert lib.quantize_act_layout(ctypes.c_void_p(64), 4, 8, 1.0, ctypes.c_void_p(72), 1, None) == -1
+
+
+@pytest.mark.parametrize("rows,cols", [(1, 1), (16, 32), (17, 33), (5, 100), (64, 768), (31, 3072)])
+def test_t16x32_layout_helpers(rows, cols):
+    # the block layout as the header defines it: element (t, c) at byte
+    # ((t / 16) * C + c / 32) * 512 + (t % 16) * 32 + c % 32, C = ceil(cols / 32)
+    rng = np.random.default_rng(rows * 1000 + cols)
+    a = rng.integers(-127, 128, (rows, cols), dtype=np.int8)
+    b = sl.to_t16x32(a, fill=99)
+    assert b.shape == sl.t16x32_shape(rows, cols)
+    flat = b.reshape(-1)
+    C = (cols + 31) // 32
+    t, c = np.meshgrid(np.arange(rows), np.arange(cols), indexing="ij")
+    off = ((t // 16) * C + c // 32) * 512 + (t % 16) * 32 + c % 32
+    assert np.array_equal(flat[off], a)
+    mask = np.ones(flat.size, bool)
+    mask[off.reshape(-1)] = False
+    assert (flat[mask] == 99).all()  # everything else is padding
+    assert np.array_equal(sl.from_t16x32(b, rows, cols), a)
