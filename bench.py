@@ -8,6 +8,10 @@ requant to int8), W2 768x3072 (dequant + bias to fp32).
 
 One step is one pass of the whole hot path over one batch: quantize_act of the
 fp32 input -> linear 1 (int8 out) -> linear 2 (fp32 out), all on one stream.
+The int8 activations between them stay in the library's 16-token x
+32-feature block layout (--layout t16x32, the default: the order the matrix
+cores read; the quantisation writes it and linear 1 writes its int8 output in
+it), or are row-major throughout (--layout rows).
 Inputs are resident in HBM when timing starts; the step rotates over enough
 input/output buffer sets (> 2x the 256 MB last-level cache) that every step
 reads its activations from HBM, not from a cache warmed by the previous step.
@@ -50,13 +54,22 @@ MALL_BYTES = 256 << 20
 COPY_CALIB_BYTES = 256 << 20  # one read and one write of this many bytes per copy launch
 COPY_CALIB_LAUNCHES = 3
 KERNEL_REPS = 50  # launches per kernel in the per-kernel timing leg
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2211_07715_amd", "csrc", "kernels.hip")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2211_07715_amd", "csrc", f)
+                  for f in ("kernels.hip", "kernels_direct.hip", "sl_device.h")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 
 def kernel_source_hash() -> str:
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for fn in KERNEL_SOURCES:
+        with open(fn, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def act_shape(sl, layout, rows, cols):
+    """Device shape of an int8 activation in the chosen layout."""
+    return sl.t16x32_shape(rows, cols) if layout == sl.LAYOUT_T16X32 else (rows, cols)
 
 
 def algorithmic_bytes(m, n, k, nnzb, out_bytes):
@@ -65,7 +78,7 @@ def algorithmic_bytes(m, n, k, nnzb, out_bytes):
     return m * k + m * n * out_bytes + nnzb * 6 + (n // 4 + 1) * 4 + 8 * n
 
 
-def chain_latency(torch, sl, wk, name, calib, stream, dev, reps=200, warmup=20):
+def chain_latency(torch, sl, wk, name, calib, stream, dev, layout, reps=200, warmup=20):
     """Latency of a workload's chain of linears (inputs resident, buffers
     reused: a warm, latency-oriented figure). Returns host-launched time per
     chain and per layer, and the same chain replayed from a HIP graph (after
@@ -79,9 +92,13 @@ def chain_latency(torch, sl, wk, name, calib, stream, dev, reps=200, warmup=20):
         packed[key] = sl.PackedWeight.pack(wd["w"], wd["sw"], wd["b"])
         kinds[key] = sl.EPI_BY_NAME[wl.op_kind(layer, op)]
         dt = torch.int8 if kinds[key] in (3, 4) else (torch.int32 if kinds[key] == 0 else torch.float32)
-        bufs[key] = torch.empty((wl.m, op.n_out), dtype=dt, device=dev)
+        shape = act_shape(sl, layout, wl.m, op.n_out) if kinds[key] in (3, 4) else (wl.m, op.n_out)
+        bufs[key] = torch.empty(shape, dtype=dt, device=dev)
         if wl.op_src(layer, op) == "seeded":
-            seeded[key] = torch.from_numpy(wk.op_seeded_x(wl, layer, op)).to(dev)
+            xs8 = wk.op_seeded_x(wl, layer, op)
+            if layout == sl.LAYOUT_T16X32:
+                xs8 = sl.to_t16x32(xs8)
+            seeded[key] = torch.from_numpy(xs8).to(dev)
 
     def chain():
         st = torch.cuda.current_stream()  # the capture stream while a graph is recorded
@@ -92,7 +109,9 @@ def chain_latency(torch, sl, wk, name, calib, stream, dev, reps=200, warmup=20):
                 xin, xs = seeded[key], float(wk.SX)
             else:
                 xin, xs = bufs[src], float(calib[src])
-            packed[key].run(xin, xs, kinds[key], out_scale=float(calib.get(key, 1.0)), out=bufs[key], stream=st)
+            yl = layout if kinds[key] in (3, 4) else sl.LAYOUT_ROWS
+            packed[key].run(xin, xs, kinds[key], out_scale=float(calib.get(key, 1.0)), out=bufs[key], stream=st,
+                            x_layout=layout, y_layout=yl, m_tokens=wl.m)
 
     for _ in range(warmup):
         chain()
@@ -105,6 +124,7 @@ def chain_latency(torch, sl, wk, name, calib, stream, dev, reps=200, warmup=20):
     torch.cuda.synchronize()
     eager_us = e0.elapsed_time(e1) / reps * 1e3
     out = {"workload": f"{wl.name}: {wl.notes}", "m_tokens": wl.m, "layers": wl.layers, "linears": len(ops),
+           "activation_layout": "t16x32" if layout == sl.LAYOUT_T16X32 else "rows",
            "chain_us": round(eager_us, 2), "per_layer_us": round(eager_us / wl.layers, 2)}
     ref = {k: v.clone() for k, v in bufs.items()}
     try:
@@ -149,6 +169,8 @@ def parse():
     p.add_argument("--steps", type=int, default=200)
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--workload", default="c1")
+    p.add_argument("--layout", choices=("t16x32", "rows"), default="t16x32",
+                   help="layout of the int8 activations between the kernels")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--cpu-seconds", type=float, default=10.0)
     p.add_argument("--no-latency", action="store_true", help="skip the DistilBERT-layer latency legs")
@@ -174,6 +196,7 @@ def main():
         sys.exit(2)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    layout = sl.LAYOUT_T16X32 if args.layout == "t16x32" else sl.LAYOUT_ROWS
 
     wl = wk.workloads()[args.workload]
     with open(os.path.join(ROOT, "tests", "golden", "calibration.json")) as f:
@@ -206,10 +229,11 @@ def main():
     sets = []
     xf_dev = torch.from_numpy(x_f32).to(dev)
     for _ in range(n_sets):
-        s = {"xf": xf_dev.clone(), "q": torch.empty((m, first.k_in), dtype=torch.int8, device=dev)}
+        s = {"xf": xf_dev.clone(), "q": torch.empty(act_shape(sl, layout, m, first.k_in), dtype=torch.int8, device=dev)}
         for md in meta:
             dt = {0: torch.int32, 1: torch.float32, 2: torch.float32, 3: torch.int8, 4: torch.int8}[md["kind"]]
-            s[md["key"]] = torch.empty((m, md["n"]), dtype=dt, device=dev)
+            shape = act_shape(sl, layout, m, md["n"]) if md["kind"] in (3, 4) else (m, md["n"])
+            s[md["key"]] = torch.empty(shape, dtype=dt, device=dev)
         sets.append(s)
     del xf_dev
     stream = torch.cuda.current_stream()
@@ -217,7 +241,7 @@ def main():
     def step(s, only=None):
         # only=j launches just kernel j of the step (0: quantize_act, 1..: the linears)
         if only is None or only == 0:
-            sl.quantize_act(s["xf"], float(sx), out=s["q"], stream=stream)
+            sl.quantize_act(s["xf"], float(sx), out=s["q"], stream=stream, layout=layout)
         for i, (pw, md) in enumerate(zip(packed, meta)):
             if only is not None and only != i + 1:
                 continue
@@ -227,7 +251,9 @@ def main():
                 src = md["src"]
                 xin = s[src]
                 xs = next(mm["so"] for mm in meta if mm["key"] == src)
-            pw.run(xin, xs, md["kind"], out_scale=md["so"], out=s[md["key"]], stream=stream)
+            yl = layout if md["kind"] in (3, 4) else sl.LAYOUT_ROWS
+            pw.run(xin, xs, md["kind"], out_scale=md["so"], out=s[md["key"]], stream=stream, x_layout=layout,
+                   y_layout=yl, m_tokens=m)
 
     n_k = 1 + len(meta)
     # every buffer set gets valid activations once (set-up, not warm-up)
@@ -303,7 +329,7 @@ def main():
             calib_all = json.load(f)
         latency = {}
         for name, label in (("c2", "bs32_seq128_80pct_layer"), ("c3_seq128_s80", "bs1_seq128_80pct_6layers")):
-            latency[label] = chain_latency(torch, sl, wk, name, calib_all[name], stream, dev)
+            latency[label] = chain_latency(torch, sl, wk, name, calib_all[name], stream, dev, layout)
 
     # ---- CPU oracle baseline on the same step (bounded by time)
     cpu = None
@@ -345,7 +371,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{wl.name}: {wl.notes}", "m_tokens": m,
                    "ops": [f"{md['key']} {md['n']}x{md['k']} kind={md['kind']} nnzb={md['nnzb']}" for md in meta],
-                   "buffer_sets": n_sets, "kernel_reps": KERNEL_REPS, "wall_s": round(wall, 3)},
+                   "activation_layout": args.layout, "buffer_sets": n_sets, "kernel_reps": KERNEL_REPS,
+                   "wall_s": round(wall, 3)},
         "kernels": kernels,
         "roofline": roofline,
         "cpu_baseline": cpu,

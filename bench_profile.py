@@ -38,7 +38,7 @@ def bench_names(workload: str):
 
 
 def _is_lib_kernel(name: str) -> bool:
-    return "sparse_linear" in name or "quantize_vec16" in name or "quantize_scalar" in name
+    return "sparse_linear" in name or "quantize_" in name
 
 
 def _rows(d: str, suffix: str):
