@@ -46,6 +46,11 @@ struct DShape {
     static constexpr int BUF = 2 * AB;
     static constexpr int LDS = D * BUF;
     static constexpr int VEC = 2 * NT * kTileN * 4;  // per compute wave: weight scales, then biases
+    // per compute wave: 16 token rows of 32 four-byte outputs (two tiles),
+    // padded to 36 words so that neither the writes nor the reads of the
+    // transpose meet a bank twice in one pass
+    static constexpr int TRW = 36;
+    static constexpr int TR = 16 * TRW * 4;
     static_assert(NT <= 32, "an overflow mask has 32 bits");
 };
 
@@ -296,6 +301,7 @@ __device__ __forceinline__ void direct_body(const LinearArgs &a, const GeluArg *
     // the item's weight scales and biases, one copy each into this wave's
     // LDS area (NT*4 lanes of 16 bytes); the epilogue waits for them
     float *vec = reinterpret_cast<float *>(smem + S::LDS + kTabBytes + wave * S::VEC);
+    int8_t *const trans = smem + S::LDS + kTabBytes + S::NW * S::VEC + wave * S::TR;
     auto fetch_vec = [&](const ItemIter &it) {
         if constexpr (KIND != SL_EPI_ACC_I32) {
             const __amdgpu_buffer_rsrc_t sr =
@@ -342,6 +348,45 @@ __device__ __forceinline__ void direct_body(const LinearArgs &a, const GeluArg *
         // in the block layout the padding tokens of the last block may be
         // written too
         const int64_t mlim = YT ? (a.m + 15) / 16 * 16 : a.m;
+        if constexpr (EpiOut<KIND>::kBytes == 4 && KIND != SL_EPI_F32_GELU && !YT && NT % 2 == 0) {
+            if (t0 + ST * 16 <= mlim && (tile0 + NT) * kTileN <= a.n) {
+                // Whole tile, int32 or fp32 outputs in rows (the fp32 GELU kind
+                // keeps the direct stores: two tiles of its temporaries at once
+                // would spill): a lane's 16 bytes sit in
+                // a different row from its quad neighbours', so each pair of
+                // tiles goes through this wave's LDS transpose area. A store
+                // then writes 8 tokens x 32 channels (128 contiguous bytes a
+                // token, 8 lanes a row).
+                int32_t *const tr = reinterpret_cast<int32_t *>(trans);
+                const int wi = (lane & 15) * S::TRW + 4 * (lane >> 4);  // write: token l%16, channels 4(l/16)..
+                const int ri = (lane >> 3) * S::TRW + 4 * (lane & 7);   // read: token l/8 (+8), channels 4(l%8)..
+                int8_t *const y8 = static_cast<int8_t *>(a.y);
+#pragma unroll
+                for (int c = 0; c < NT; c += 2) {
+                    float s0[4], b0[4], s1[4], b1[4];
+                    scales(c, s0, b0);
+                    scales(c + 1, s1, b1);
+#pragma unroll
+                    for (int st = 0; st < ST; ++st) {
+                        const i32x4 v0 = __builtin_bit_cast(
+                            i32x4, epilogue_value<KIND>(a, acc[c][st], s0, b0, tab, hinv, eoff, cmax));
+                        const i32x4 v1 = __builtin_bit_cast(
+                            i32x4, epilogue_value<KIND>(a, acc[c + 1][st], s1, b1, tab, hinv, eoff, cmax));
+                        // (a wave's LDS operations take effect in order: the
+                        // previous pair's reads are done before these writes)
+                        *reinterpret_cast<i32x4 *>(tr + wi) = v0;
+                        *reinterpret_cast<i32x4 *>(tr + wi + 16) = v1;
+                        const i32x4 r0 = *reinterpret_cast<const i32x4 *>(tr + ri);
+                        const i32x4 r1 = *reinterpret_cast<const i32x4 *>(tr + ri + 8 * S::TRW);
+                        const int64_t row = t0 + st * 16 + (lane >> 3);
+                        int8_t *const p = y8 + (row * a.n + (tile0 + c) * kTileN + 4 * (lane & 7)) * 4;
+                        *reinterpret_cast<i32x4 *>(p) = r0;
+                        *reinterpret_cast<i32x4 *>(p + (int64_t)8 * a.n * 4) = r1;
+                    }
+                }
+                return;
+            }
+        }
         if (t0 + ST * 16 <= mlim && (tile0 + NT) * kTileN <= a.n) {
             // whole tile: a uniform base and a lane offset, no bounds checks
             using T = typename EpiOut<KIND>::T;
@@ -492,8 +537,9 @@ static sl_status launch_direct_cfg(const LinearArgs &a, const GeluArg *ep, hipSt
         fn = reinterpret_cast<const void *>(&sparse_linear_direct_gelu_kernel<ST, NT, WM, D, XT, YT>);
     else
         fn = reinterpret_cast<const void *>(&sparse_linear_direct_kernel<KIND, ST, NT, WM, D, XT, YT>);
-    const size_t lds = (size_t)S::LDS + S::NW * S::VEC + (KIND == SL_EPI_I8_GELU ? kGeluLds : 0);
-    static_assert(S::LDS + S::NW * S::VEC + kGeluLds <= kLdsMax, "workgroup shape exceeds LDS");
+    constexpr size_t kTrans = EpiOut<KIND>::kBytes == 4 && KIND != SL_EPI_F32_GELU && !YT ? S::NW * S::TR : 0;
+    const size_t lds = (size_t)S::LDS + S::NW * S::VEC + kTrans + (KIND == SL_EPI_I8_GELU ? kGeluLds : 0);
+    static_assert(S::LDS + S::NW * (S::VEC + S::TR) + kGeluLds <= kLdsMax, "workgroup shape exceeds LDS");
     static int resident[kMaxDevices] = {};  // per kernel instance and device
     int grid = 0;
     const sl_status st = persistent_grid(fn, S::NTHG, lds, resident, &grid);
