@@ -42,7 +42,7 @@ EXPORTS = ("sparse_linear_pack", "sparse_linear_pack_host", "sparse_linear_run",
            "quantize_act", "quantize_act_layout",
            "sparse_linear_unpack", "sparse_linear_info", "sparse_linear_export_bsr",
            "sparse_linear_tile_stats", "sparse_linear_free", "sl_status_string", "sl_last_error",
-           "sl_abi_version")
+           "sl_abi_version", "sl_last_path")
 
 _lib: Optional[ctypes.CDLL] = None
 
@@ -86,6 +86,8 @@ def load() -> ctypes.CDLL:
     lib.sl_last_error.restype = ctypes.c_char_p
     lib.sl_abi_version.argtypes = []
     lib.sl_abi_version.restype = i32
+    lib.sl_last_path.argtypes = []
+    lib.sl_last_path.restype = ctypes.c_char_p
     _lib = lib
     return lib
 
@@ -235,6 +237,11 @@ class PackedWeight:
                                                ctypes.c_void_p(out.data_ptr()), int(y_layout), _stream_ptr(stream)),
                "sparse_linear_run_layout")
         return out
+
+
+def last_path() -> str:
+    """Kernel and workgroup shape of the last successful run on this thread."""
+    return load().sl_last_path().decode()
 
 
 def quantize_act(x, scale: float, out=None, stream=None, layout: int = LAYOUT_ROWS):

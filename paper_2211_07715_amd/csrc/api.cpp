@@ -13,6 +13,11 @@ namespace sl {
 static thread_local std::string g_last_error;
 
 void set_error(const std::string &msg) { g_last_error = msg; }
+std::string &last_path()
+{
+    static thread_local std::string p;
+    return p;
+}
 void clear_error() { g_last_error.clear(); }
 
 }  // namespace sl
@@ -269,5 +274,7 @@ const char *sl_status_string(int32_t s)
 const char *sl_last_error(void) { return g_last_error.c_str(); }
 
 int32_t sl_abi_version(void) { return SL_ABI_VERSION; }
+
+const char *sl_last_path(void) { return sl::last_path().c_str(); }
 
 }  // extern "C"

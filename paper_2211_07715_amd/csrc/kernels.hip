@@ -676,6 +676,38 @@ sl_status upload_image(sl_packed_weight *w)
                 om[((size_t)wi * ncg + g) * 2 + 1] = pp[0];
             }
     }
+    // weight panels, one table per tile-group size of the weight-stationary shapes
+    std::vector<int> pnts;
+    for (const PanelCfg &c : kPanelCfgs)
+        if (std::find(pnts.begin(), pnts.end(), c.nt) == pnts.end()) pnts.push_back(c.nt);
+    if ((int)pnts.size() > kMaxPanTables) {
+        set_error("internal: too many weight-panel sizes");
+        return SL_ERR_UNSUPPORTED;
+    }
+    std::vector<std::vector<uint32_t>> pans(pnts.size());
+    std::vector<uint32_t> pan_max(pnts.size(), 0);
+    for (size_t i = 0; i < pnts.size(); ++i) {
+        const int nt = pnts[i];
+        const int ncg = (ti.n_tiles + nt - 1) / nt;
+        std::vector<uint32_t> &pt = pans[i];
+        pt.assign((size_t)ncg * (ti.n_win + 1) * 4, 0u);
+        for (int g = 0; g < ncg; ++g) {
+            const int t0 = g * nt, ntl = std::min(nt, ti.n_tiles - t0);
+            uint64_t base = 0;
+            for (int wi = 0; wi < ti.n_win; ++wi) {
+                const uint32_t *pp = ti.ovf_ptr.data() + (size_t)wi * pstride + t0;
+                uint32_t mask = 0;
+                for (int j = 0; j < ntl; ++j) mask |= (pp[j + 1] > pp[j] ? 1u : 0u) << j;
+                uint32_t *e = &pt[((size_t)g * (ti.n_win + 1) + wi) * 4];
+                e[0] = mask;
+                e[1] = pp[0];
+                e[2] = (uint32_t)std::min<uint64_t>(base, UINT32_MAX);
+                base += (uint64_t)(nt + __builtin_popcount(mask)) * kOpPieces;
+            }
+            pt[((size_t)g * (ti.n_win + 1) + ti.n_win) * 4 + 2] = (uint32_t)std::min<uint64_t>(base, UINT32_MAX);
+            pan_max[i] = (uint32_t)std::min<uint64_t>(std::max<uint64_t>(pan_max[i], base), UINT32_MAX);
+        }
+    }
     const size_t b_main = std::max<size_t>(ti.main.size(), 16);
     const size_t b_ovf = std::max<size_t>(ti.ovf.size(), 16);
     const size_t b_vec = (size_t)w->n_out * sizeof(float);
@@ -688,6 +720,11 @@ sl_status upload_image(sl_packed_weight *w)
     for (size_t i = 0; i < nts.size(); ++i) {
         o_om[i] = o_end;
         o_end = align256(o_end + oms[i].size() * sizeof(uint32_t));
+    }
+    std::vector<size_t> o_pan(pnts.size());
+    for (size_t i = 0; i < pnts.size(); ++i) {
+        o_pan[i] = o_end;
+        o_end = align256(o_end + pans[i].size() * sizeof(uint32_t));
     }
     const size_t total = o_end;
     void *base = nullptr;
@@ -710,6 +747,15 @@ sl_status upload_image(sl_packed_weight *w)
         w->dev.om[i] = reinterpret_cast<const uint32_t *>(p + o_om[i]);
     }
     w->dev.n_om = (int32_t)nts.size();
+    for (size_t i = 0; i < pnts.size(); ++i) {
+        HIP_TRY(hipMemcpy(p + o_pan[i], pans[i].data(), pans[i].size() * sizeof(uint32_t), hipMemcpyHostToDevice));
+        w->dev.pan_nt[i] = pnts[i];
+        w->dev.pan_pieces[i] = (int32_t)std::min<uint32_t>(pan_max[i], INT32_MAX);
+        w->dev.pan[i] = reinterpret_cast<const uint32_t *>(p + o_pan[i]);
+    }
+    w->dev.n_pan = (int32_t)pnts.size();
+    w->dev.img_bytes = (uint32_t)(o_ovf + ti.ovf.size());
+    w->dev.ovf_off = (uint32_t)o_ovf;
     w->dev.main = reinterpret_cast<const int8_t *>(p + o_main);
     w->dev.ovf = reinterpret_cast<const int8_t *>(p + o_ovf);
     w->dev.ovf_ptr = nullptr;
@@ -884,6 +930,89 @@ static DirectCfg choose_direct_cfg(int64_t m, const sl_packed_weight *w)
     return best ? *best : *most;
 }
 
+// The weight-stationary shape the default path uses: 96 channels x 32
+// tokens per wave, 8 waves.
+static const PanelCfg kPanelDefault{6, 2, 8, 2};
+
+// Weight-stationary shape for a launch of a.m tokens: the compiled shapes
+// whose largest panel fits in LDS are scored by the bytes their workgroups
+// read (token rows once per channel group, the panel once per workgroup)
+// spread over the CUs they keep busy (only: consider that shape alone);
+// SL_PTILE="nt,st,nwv,r" overrides. Fills a's channel-group and slice
+// fields; SL_ERR_UNSUPPORTED when no panel fits.
+static sl_status choose_panel_cfg(LinearArgs &a, const sl_packed_weight *w, int32_t run_kind, bool yt, PanelCfg *out,
+                                  size_t *lds_out, const PanelCfg *only)
+{
+    int n_cu = 0, dev = 0;
+    HIP_TRY(hipGetDevice(&dev));
+    HIP_TRY(hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev));
+    const char *env = getenv("SL_PTILE");
+    PanelCfg forced{};
+    const bool have_forced =
+        env && sscanf(env, "%d,%d,%d,%d", &forced.nt, &forced.st, &forced.nwv, &forced.r) == 4;
+    const int64_t mpad = (a.m + 15) / 16 * 16;
+    double best_cost = 0;
+    bool found = false;
+    for (int ci = 0; ci < kNumPanelCfgs; ++ci) {
+        const PanelCfg c = kPanelCfgs[ci];
+        if (have_forced && (c.nt != forced.nt || c.st != forced.st || c.nwv != forced.nwv || c.r != forced.r))
+            continue;
+        if (only && (c.nt != only->nt || c.st != only->st || c.nwv != only->nwv || c.r != only->r)) continue;
+        int pi = -1;
+        for (int i = 0; i < w->dev.n_pan; ++i)
+            if (w->dev.pan_nt[i] == c.nt) pi = i;
+        if (pi < 0) continue;
+        const int32_t pieces = w->dev.pan_pieces[pi];
+        const size_t lds = panel_lds_bytes(c, run_kind, yt, w->tiles.n_win, pieces);
+        if (lds > kLdsMax) continue;
+        // resident workgroups per device, cached per (device, shape, LDS size)
+        static thread_local struct {
+            int dev, ci;
+            size_t lds;
+            int res;
+        } cache[16];
+        static thread_local int cache_n = 0;
+        int res = -1;
+        for (int i = 0; i < cache_n; ++i)
+            if (cache[i].dev == dev && cache[i].ci == ci && cache[i].lds == lds) res = cache[i].res;
+        if (res < 0) {
+            const sl_status st = panel_resident(c, lds, &res);
+            if (st != SL_OK) return st;
+            cache[cache_n % 16] = {dev, ci, lds, res};
+            cache_n = cache_n < 16 ? cache_n + 1 : 16;
+        }
+        if (res < 1) continue;
+        const int64_t n_cg = (w->tiles.n_tiles + c.nt - 1) / c.nt;
+        const int64_t groups = (mpad + c.tg() - 1) / c.tg();
+        // slices: enough workgroups to fill the resident slots once
+        const int64_t want = std::max<int64_t>(1, res / n_cg);
+        const int64_t sg = std::max<int64_t>(1, (groups + want - 1) / want);
+        const int64_t n_sl = (groups + sg - 1) / sg;
+        const int64_t nwg = n_cg * n_sl;
+        if (nwg > 0x7fffffff) continue;
+        // busy CUs and the bytes each reads
+        const double cus = (double)std::min<int64_t>(n_cu, nwg);
+        const double bytes = (double)a.m * w->k_in * n_cg + (double)nwg * pieces * 16.0;
+        // waves per workgroup without a token group idle
+        const double wave_use = std::min(1.0, (double)sg / c.nwv);
+        const double cost = bytes / cus / wave_use;
+        if (!found || cost < best_cost) {
+            found = true;
+            best_cost = cost;
+            *out = c;
+            *lds_out = lds;
+            a.n_cgroups = (int32_t)n_cg;
+            a.n_slices = (int32_t)n_sl;
+            a.slice_groups = (int32_t)sg;
+            a.pan = w->dev.pan[pi];
+        }
+    }
+    if (!found) return SL_ERR_UNSUPPORTED;
+    a.img_bytes = w->dev.img_bytes;
+    a.ovf_off = w->dev.ovf_off;
+    return SL_OK;
+}
+
 sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int32_t x_layout, int64_t m, float sx,
                         int32_t kind, float inv_so, void *y, int32_t y_layout, void *stream)
 {
@@ -908,6 +1037,11 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int32_t x_la
     a.inv_so = inv_so;
     a.n_tiles = ti.n_tiles;
     a.n_win = ti.n_win;
+    a.pan = nullptr;
+    a.img_bytes = 0;
+    a.ovf_off = 0;
+    a.n_slices = 0;
+    a.slice_groups = 0;
     hipStream_t s = static_cast<hipStream_t>(stream);
 
     GeluArg ga;
@@ -937,12 +1071,37 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int32_t x_la
         a.y = static_cast<char *>(y) + (yt ? t0 / 16 * a.y_cb * 512 : t0 * w->n_out * out_bytes);
         a.m = std::min(chunk, m - t0);
         const bool vec = xt || ((w->k_in % 16 == 0) && ((reinterpret_cast<uintptr_t>(a.x) & 15) == 0));
-        // Block-layout input, or a block-layout output from aligned rows: the
-        // direct-operand kernel. Row-major input and output: the staged
-        // kernel, unless SL_PATH=direct selects the direct one for aligned
-        // rows (tests, tuning).
+        // Aligned or block-layout rows: the weight-stationary kernel where it
+        // pays (its 96-channel panel fits in LDS and every wave of a
+        // workgroup gets at least two token groups, evenly), else the
+        // direct-operand kernel (block-layout input, or block-layout output
+        // from aligned rows) or the staged kernel (row-major input and
+        // output). SL_PATH=panel|direct|staged forces a kernel (tests,
+        // tuning; panel falls back when no panel fits).
         const char *path = getenv("SL_PATH");
-        const bool direct = xt || (yt && vec) || (vec && path && strcmp(path, "direct") == 0);
+        const bool force_panel = path && strcmp(path, "panel") == 0;
+        const bool auto_path = !path || !*path;
+        if (vec && (force_panel || auto_path)) {
+            PanelCfg pc{};
+            size_t lds = 0;
+            sl_status pst = choose_panel_cfg(a, w, run_kind, yt, &pc, &lds, force_panel ? nullptr : &kPanelDefault);
+            if (pst == SL_OK && !force_panel &&
+                !(a.slice_groups >= 2 * pc.nwv && (a.slice_groups % pc.nwv == 0 || a.slice_groups >= 8 * pc.nwv)))
+                pst = SL_ERR_UNSUPPORTED;
+            if (pst == SL_OK) {
+                pst = launch_panel(a, run_kind == SL_EPI_I8_GELU ? &ga : nullptr, run_kind, pc, xt, yt, lds, s);
+                if (pst != SL_OK) return pst;
+                last_path() = "panel " + std::to_string(pc.nt) + "," + std::to_string(pc.st) + "," +
+                              std::to_string(pc.nwv) + "," + std::to_string(pc.r) +
+                              " groups=" + std::to_string(a.n_cgroups) +
+                              " slices=" + std::to_string(a.n_slices) + "x" + std::to_string(a.slice_groups) +
+                              " lds=" + std::to_string(lds);
+                continue;
+            }
+            if (pst != SL_ERR_UNSUPPORTED) return pst;
+        }
+        const bool direct = (xt || (yt && vec) || (vec && path && strcmp(path, "direct") == 0)) &&
+                            !(path && strcmp(path, "staged") == 0 && !xt && !yt);
         TileCfg cfg{};
         DirectCfg dcfg{};
         int nt, tm;
@@ -972,7 +1131,11 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int32_t x_la
         sl_status st;
         if (direct) {
             st = launch_direct(a, run_kind == SL_EPI_I8_GELU ? &ga : nullptr, run_kind, dcfg, xt, yt, s);
+            last_path() = "direct " + std::to_string(dcfg.st) + "," + std::to_string(dcfg.nt) + "," +
+                          std::to_string(dcfg.wm) + "," + std::to_string(dcfg.d);
         } else {
+            last_path() = "staged " + std::to_string(cfg.st) + "," + std::to_string(cfg.ct) + "," +
+                          std::to_string(cfg.wm) + "," + std::to_string(cfg.wn) + "," + std::to_string(cfg.d);
             switch (run_kind) {
             case SL_EPI_ACC_I32: st = launch_vec<SL_EPI_ACC_I32>(a, nullptr, cfg, s, vec, yt); break;
             case SL_EPI_F32: st = launch_vec<SL_EPI_F32>(a, nullptr, cfg, s, vec, yt); break;

@@ -57,6 +57,12 @@ struct LinearArgs {
     int64_t n_items;    // work items: token tiles x channel groups
     int32_t x_cb;       // 32-feature column blocks of x (SL_LAYOUT_T16X32 input)
     int32_t y_cb;       // 32-channel column blocks of y (SL_LAYOUT_T16X32 output)
+    // weight-stationary kernel only
+    const uint32_t *pan;    // panel table of this launch's tile-group size, [n_cgroups][n_win + 1][4]
+    uint32_t img_bytes;     // main image through the end of the overflow operands
+    uint32_t ovf_off;       // byte offset of the overflow operands from main
+    int32_t n_slices;       // token slices per channel group
+    int32_t slice_groups;   // token groups (16 ST tokens) per slice
 };
 
 // Byte offset of element (t, c) of an int8 tensor in SL_LAYOUT_T16X32 with
@@ -270,6 +276,24 @@ extern const DirectCfg kDirectCfgs[kNumDirectCfgs];
 // SL_EPI_I8_GELU; xt / yt: x / y in SL_LAYOUT_T16X32 (yt for int8 kinds)
 sl_status launch_direct(const LinearArgs &a, const GeluArg *ep, int32_t run_kind, DirectCfg c, bool xt, bool yt,
                         hipStream_t stream);
+
+// Workgroup shapes of the weight-stationary kernel (kernels_panel.hip): NWV
+// waves, each multiplying ST 16-token subtiles by the NT 16-channel tiles of
+// the workgroup's channel group, whose whole weight panel sits in LDS; R
+// windows of token rows in each wave's registers.
+struct PanelCfg {
+    int nt, st, nwv, r;
+    int tg() const { return 16 * st; }
+};
+constexpr int kNumPanelCfgs = 6;
+extern const PanelCfg kPanelCfgs[kNumPanelCfgs];
+// LDS bytes of a panel kernel launch holding `pieces` 16-byte panel pieces
+size_t panel_lds_bytes(PanelCfg c, int32_t run_kind, bool yt, int32_t n_win, int32_t pieces);
+sl_status launch_panel(const LinearArgs &a, const GeluArg *ep, int32_t run_kind, PanelCfg c, bool xt, bool yt,
+                       size_t lds, hipStream_t stream);
+// resident workgroups of a panel-kernel shape for `lds` bytes of LDS (all kinds and layouts of a
+// shape share one register budget; the SL_EPI_F32 row-major instance stands for them)
+sl_status panel_resident(PanelCfg c, size_t lds, int *out);
 
 // Persistent grid size of a kernel on the current device: the workgroups of
 // `threads` threads and `lds` bytes of dynamic LDS resident at once. On first

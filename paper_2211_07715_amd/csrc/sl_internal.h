@@ -70,7 +70,15 @@ std::shared_ptr<const GeluTable> gelu_table(float inv_so);
 // group g, the pair (mask, first): bit j of mask set if tile g*nt + j has an
 // overflow operand in window w; first = index of the group's first overflow
 // operand of the window. Layout [n_win][n_groups][2] uint32.
-constexpr int kMaxOmTables = 4;
+constexpr int kMaxOmTables = 8;
+
+// Weight panels of the weight-stationary kernel, per tile-group size nt: for
+// channel group g and window w, the entry {mask, first, base, 0} at
+// [g][n_win + 1][4] uint32: mask and first as in the overflow table; base =
+// offset, in 16-byte pieces, of the window's operands in the group's panel
+// (the nt main operands, then the window's overflow operands in tile order).
+// Entry n_win holds the panel's total size in its base word.
+constexpr int kMaxPanTables = 4;
 
 struct DeviceImage {
     int device = -1;
@@ -83,6 +91,12 @@ struct DeviceImage {
     int32_t n_om = 0;
     int32_t om_nt[kMaxOmTables] = {};
     const uint32_t *om[kMaxOmTables] = {};
+    int32_t n_pan = 0;
+    int32_t pan_nt[kMaxPanTables] = {};
+    int32_t pan_pieces[kMaxPanTables] = {};  // largest panel over the groups, 16-byte pieces
+    const uint32_t *pan[kMaxPanTables] = {};
+    uint32_t img_bytes = 0;  // main image through the end of the overflow operands
+    uint32_t ovf_off = 0;    // byte offset of the overflow operands from the main image
     int64_t bytes = 0;
 };
 
@@ -104,6 +118,9 @@ struct sl_packed_weight {
 };
 
 namespace sl {
+
+// thread-local name of the last launched kernel shape (sl_last_path)
+std::string &last_path();
 
 // thread-local error text
 void set_error(const std::string &msg);

@@ -68,9 +68,11 @@ SMALL = [(1, 4, 1), (3, 16, 7), (16, 16, 64), (17, 20, 100), (64, 48, 768), (65,
          (33, 32, 3072), (130, 1024, 4096), (5, 12, 2049)]
 
 
-# kernel paths: the default choice (the staged kernel for row-major token
-# rows) and the direct-operand kernel in each of its workgroup shapes
-PATHS = {"default": {}, "direct": {"SL_PATH": "direct"},
+# kernel paths: the default choice (the weight-stationary kernel where it
+# pays, else the staged kernel for row-major token rows), the staged kernel
+# forced, and the direct-operand kernel in each of its workgroup shapes (the
+# weight-stationary shapes are covered in test_gpu_panel.py)
+PATHS = {"default": {}, "staged": {"SL_PATH": "staged"}, "direct": {"SL_PATH": "direct"},
          "direct_64x96": {"SL_PATH": "direct", "SL_DTILE": "1,6,4,6"},
          "direct_64x32": {"SL_PATH": "direct", "SL_DTILE": "1,2,4,8"},
          "direct_128x96": {"SL_PATH": "direct", "SL_DTILE": "2,6,4,4"}}
