@@ -20,7 +20,8 @@ Prints ONE JSON line. ``value`` is effective int8 TOPS over non-zero MACs
 (2 * M * 4 * stored_blocks per linear, summed) per step time; the K timed
 steps are bracketed by two HIP events on the launch stream. Afterwards each
 kernel of the step is launched KERNEL_REPS times back to back (same rotating
-buffers) between two events, which gives its average launch duration.
+buffers) from a captured HIP graph, between two events, which gives its
+average launch duration free of host launch cost.
 ``roofline`` describes the slowest kernel against the HBM bound: its
 algorithmic bytes (X + Y + canonical packed W + scales) per launch divided by
 that duration; ``traffic`` is the counter-measured bytes per launch from
@@ -31,8 +32,9 @@ seq 128 and the 6-layer stack at batch 1 x seq 128 (80 % sparsity, warm,
 host-launched and replayed from a HIP graph).
 
 Launch order (used to match profiler dispatches to ops): one step per buffer
-set (set-up), W warm-up steps, K timed steps, then KERNEL_REPS launches of
-each kernel in step order; with --copy-calib, three elementwise copies last.
+set (set-up), W warm-up steps, K timed steps, then, per kernel in step order,
+LEG_REPLAYS replays of a graph of KERNEL_REPS launches; with --copy-calib,
+three elementwise copies last.
 """
 from __future__ import annotations
 
@@ -53,9 +55,10 @@ MFMA_I8_PEAK_TOPS = 5000.0   # MI355X dense int8 matrix peak, published
 MALL_BYTES = 256 << 20
 COPY_CALIB_BYTES = 256 << 20  # one read and one write of this many bytes per copy launch
 COPY_CALIB_LAUNCHES = 3
-KERNEL_REPS = 50  # launches per kernel in the per-kernel timing leg
+KERNEL_REPS = 50  # launches per kernel in the per-kernel timing leg (one graph)
+LEG_REPLAYS = 2   # replays of each kernel's graph; the last one is timed
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2211_07715_amd", "csrc", f)
-                  for f in ("kernels.hip", "kernels_direct.hip", "sl_device.h")]
+                  for f in ("kernels.hip", "kernels_direct.hip", "kernels_panel.hip", "sl_device.h", "gelu_table.cpp")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 
@@ -238,7 +241,7 @@ def main():
     del xf_dev
     stream = torch.cuda.current_stream()
 
-    def step(s, only=None):
+    def step(s, only=None, stream=stream):
         # only=j launches just kernel j of the step (0: quantize_act, 1..: the linears)
         if only is None or only == 0:
             sl.quantize_act(s["xf"], float(sx), out=s["q"], stream=stream, layout=layout)
@@ -276,17 +279,27 @@ def main():
     ms_per_step = e_start.elapsed_time(e_end) / args.steps
 
     # ---- per-kernel launch duration: each kernel of the step alone, KERNEL_REPS
-    # launches back to back over the rotating buffer sets, HIP events on the
-    # launch stream around the group
+    # launches back to back over the rotating buffer sets, captured in a HIP
+    # graph (host launch cost would otherwise hide a kernel shorter than it);
+    # the graph is replayed LEG_REPLAYS times and the last replay is timed
+    # with HIP events on the stream it runs on
     per_kernel_us = np.zeros(n_k)
+    cap = torch.cuda.Stream()
     for j in range(n_k):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=cap):
+            for i in range(KERNEL_REPS):
+                step(sets[i % n_sets], only=j, stream=cap)
         ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        ev0.record(stream)
-        for i in range(KERNEL_REPS):
-            step(sets[i % n_sets], only=j)
-        ev1.record(stream)
+        with torch.cuda.stream(cap):
+            for r in range(LEG_REPLAYS):
+                if r == LEG_REPLAYS - 1:
+                    ev0.record(cap)
+                g.replay()
+            ev1.record(cap)
         torch.cuda.synchronize()
         per_kernel_us[j] = ev0.elapsed_time(ev1) / KERNEL_REPS * 1e3
+        del g
 
     # ---- metric
     total_ops = sum(2 * m * 4 * md["nnzb"] for md in meta)
@@ -371,7 +384,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{wl.name}: {wl.notes}", "m_tokens": m,
                    "ops": [f"{md['key']} {md['n']}x{md['k']} kind={md['kind']} nnzb={md['nnzb']}" for md in meta],
-                   "activation_layout": args.layout, "buffer_sets": n_sets, "kernel_reps": KERNEL_REPS,
+                   "activation_layout": args.layout, "buffer_sets": n_sets, "kernel_reps": KERNEL_REPS, "leg_replays": LEG_REPLAYS,
                    "wall_s": round(wall, 3)},
         "kernels": kernels,
         "roofline": roofline,

@@ -73,12 +73,12 @@ def _map_by_order(dispatches, names, bl):
     {name: [values in the per-kernel leg]}, {name: kernel symbol}).
 
     Bench launch order: one step per buffer set, W warm-up steps, K timed
-    steps (each step: the n_k kernels in order), then KERNEL_REPS launches of
-    each kernel in step order."""
+    steps (each step: the n_k kernels in order), then, per kernel in step
+    order, LEG_REPLAYS replays of a graph of KERNEL_REPS launches."""
     dispatches = sorted(dispatches)
     n_k = len(names)
     sets, warm, steps = bl["config"]["buffer_sets"], bl["warmup"], bl["steps"]
-    reps = bl["config"]["kernel_reps"]
+    reps = bl["config"]["kernel_reps"] * bl["config"].get("leg_replays", 1)
     n_step = (sets + warm + steps) * n_k
     if len(dispatches) != n_step + reps * n_k:
         raise SystemExit(f"{len(dispatches)} library dispatches, expected {n_step + reps * n_k}")

@@ -58,9 +58,10 @@ static float unord(int32_t o)
 
 static int cell_of(const GeluTable &t, float y)
 {
-    const float c = fmaf(y, t.hinv, t.off);
-    int i = c >= 2147483520.0f ? INT32_MAX : (c <= -2147483520.0f ? INT32_MIN : (int)c);
-    return i < 0 ? 0 : (i > t.nc - 1 ? t.nc - 1 : i);
+    float c = fmaf(y, t.hinv, t.off);
+    const float top = kGeluBase + (float)(t.nc - 1);
+    c = c < kGeluBase ? kGeluBase : (c > top ? top : c);
+    return (int)(c - kGeluBase);
 }
 
 // smallest y in [lo, hi] (as fp32, ordered) with pred(y) true; pred monotone
@@ -87,7 +88,8 @@ static std::shared_ptr<GeluTable> build(float inv_so)
     t->nc = kGeluCells;
     const float h = (hi - kLo) / (float)t->nc;
     t->hinv = 1.0f / h;
-    t->off = -kLo * t->hinv;
+    // an integer offset keeps off exact next to kGeluBase
+    t->off = kGeluBase + floorf(-kLo * t->hinv);
     t->ok = false;
     if (!(isfinite(t->hinv) && isfinite(t->off))) return t;
     if (code_of(kLo, inv_so) != 0 || code_of(-1e30f, inv_so) != 0) return t;

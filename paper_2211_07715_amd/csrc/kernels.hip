@@ -128,7 +128,7 @@ __device__ __forceinline__ void sparse_linear_body(const LinearArgs &a, const Ge
         for (int u = copier ? ep->nc : tid; u < ep->nc; u += S::NTH) tab[u] = ep->cell[u];
         hinv = ep->hinv;
         eoff = ep->off;
-        cmax = (float)(ep->nc - 1);
+        cmax = kGeluBase + (float)(ep->nc - 1);
     }
 
     // Software pipeline over the element stream, one barrier per element. In

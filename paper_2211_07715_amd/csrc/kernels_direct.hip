@@ -88,7 +88,7 @@ __device__ __forceinline__ void direct_body(const LinearArgs &a, const GeluArg *
         for (int u = copier ? ep->nc : tid; u < ep->nc; u += S::NTH) tab[u] = ep->cell[u];
         hinv = ep->hinv;
         eoff = ep->off;
-        cmax = (float)(ep->nc - 1);
+        cmax = kGeluBase + (float)(ep->nc - 1);
     }
 
     // Pipeline over the (item, window) elements, one barrier per element. In

@@ -31,7 +31,7 @@ template <int NT, int ST, int NWV>
 struct PShape {
     static constexpr int NTH = 64 * NWV;
     static constexpr int TG = 16 * ST;             // tokens per group
-    static constexpr int VEC = 2 * NT * kTileN * 4;  // the group's weight scales, then its biases
+    static constexpr int VEC = 2 * NT * kTileN * 4;  // the group's scales sx * sw[n], then its biases
     // per wave: 16 token rows of 32 four-byte outputs (two tiles), padded to
     // 36 words so that neither the writes nor the reads of the transpose meet
     // a bank twice in one pass
@@ -40,11 +40,13 @@ struct PShape {
     static_assert(NT <= 32, "an overflow mask has 32 bits");
 };
 
-// int32 / fp32 outputs in rows go through a per-wave LDS transpose
+// int32 / fp32 outputs in rows, and int8 outputs in the block layout, go
+// through a per-wave LDS transpose
 template <int KIND, bool YT, int NT>
 constexpr bool panel_transposes()
 {
-    return EpiOut<KIND>::kBytes == 4 && KIND != SL_EPI_F32_GELU && !YT && NT % 2 == 0;
+    return NT % 2 == 0 && ((EpiOut<KIND>::kBytes == 4 && KIND != SL_EPI_F32_GELU && !YT) ||
+                           (EpiOut<KIND>::kBytes == 1 && YT));
 }
 
 // LDS layout: weight scales and biases | GELU step table | per-wave transpose
@@ -106,7 +108,8 @@ __device__ __forceinline__ void panel_body(const LinearArgs &a, const GeluArg *e
     if constexpr (KIND != SL_EPI_ACC_I32) {
         for (int i = tid; i < NT * kTileN; i += S::NTH) {
             const int32_t ch = tile0 * kTileN + i;
-            vec[i] = ch < a.n ? a.w_scale[ch] : 0.0f;
+            // the dequantisation scale sx * sw[n], one fp32 product as in the definition
+            vec[i] = ch < a.n ? a.sx * a.w_scale[ch] : 0.0f;
             vec[NT * kTileN + i] = ch < a.n ? a.bias[ch] : 0.0f;
         }
     }
@@ -115,7 +118,7 @@ __device__ __forceinline__ void panel_body(const LinearArgs &a, const GeluArg *e
         for (int u = tid; u < ep->nc; u += S::NTH) tab[u] = ep->cell[u];
         hinv = ep->hinv;
         eoff = ep->off;
-        cmax = (float)(ep->nc - 1);
+        cmax = kGeluBase + (float)(ep->nc - 1);
     }
     __syncthreads();
 
@@ -123,33 +126,49 @@ __device__ __forceinline__ void panel_body(const LinearArgs &a, const GeluArg *e
     // w with base(w) <= p < base(w+1): main operand pieces of tiles tile0 ..
     // (zeros past the last tile), then the window's overflow operands. Copy
     // instruction j of the workgroup moves pieces 64j .. 64j+63 (global to
-    // LDS, no registers); wave v issues instructions v, v + NWV, ...
+    // LDS, no registers); wave v issues instructions v, v + NWV, ... All
+    // source offsets are worked out first: an LDS read between the copies
+    // would make each copy wait for the ones before it.
     {
+        constexpr int kMaxCopies = (int)((kLdsMax / 1024 + NWV - 1) / NWV);
         const __amdgpu_buffer_rsrc_t ir =
             __builtin_amdgcn_make_buffer_rsrc((void *)a.main, 0, (int)a.img_bytes, kRsrcWord3);
         const uint32_t total = wtab[a.n_win].z;
         const int n_instr = (int)((total + 63) / 64);
+        uint32_t offs[kMaxCopies];
         int cw = 0;  // this lane's window cursor: pieces only grow
-        for (int j = wave; j < n_instr; j += NWV) {
-            const uint32_t p = (uint32_t)j * 64 + (uint32_t)lane;
-            while (cw + 1 < a.n_win && p >= wtab[cw + 1].z) ++cw;
-            const uint4 e = wtab[cw];
-            const uint32_t q = p - e.z;
+#pragma unroll
+        for (int i = 0; i < kMaxCopies; ++i) {
+            const int j = wave + i * NWV;
             uint32_t off = kOob;
-            if (p < total) {
-                if (q < (uint32_t)(NT * kOpPieces)) {
-                    const uint32_t t = q / kOpPieces;
-                    if (tile0 + (int32_t)t < a.n_tiles)
-                        off = ((uint32_t)(cw * a.n_tiles + tile0) * kOpPieces + q) * 16u;
-                } else {
-                    off = a.ovf_off + (e.y * kOpPieces + (q - NT * kOpPieces)) * 16u;
+            if (j < n_instr) {
+                const uint32_t p = (uint32_t)j * 64 + (uint32_t)lane;
+                while (cw + 1 < a.n_win && p >= wtab[cw + 1].z) ++cw;
+                const uint4 e = wtab[cw];
+                const uint32_t q = p - e.z;
+                if (p < total) {
+                    if (q < (uint32_t)(NT * kOpPieces)) {
+                        const uint32_t t = q / kOpPieces;
+                        if (tile0 + (int32_t)t < a.n_tiles)
+                            off = ((uint32_t)(cw * a.n_tiles + tile0) * kOpPieces + q) * 16u;
+                    } else {
+                        off = a.ovf_off + (e.y * kOpPieces + (q - NT * kOpPieces)) * 16u;
+                    }
                 }
             }
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(ir, (lds_void *)(panel + (size_t)j * 1024), 16, off, 0, 0, 0);
+            offs[i] = off;
         }
-        __builtin_amdgcn_s_waitcnt(0);
+#pragma unroll
+        for (int i = 0; i < kMaxCopies; ++i) {
+            const int j = wave + i * NWV;
+            if (j < n_instr)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(ir, (lds_void *)(panel + (size_t)j * 1024), 16, offs[i], 0,
+                                                         0, 0);
+        }
     }
-    __syncthreads();
+    // (the first token rows load while the panel copies are in flight; the
+    // wait for the copies comes after them)
+    asm volatile("" ::: "memory");
 
     // ---- token groups of this workgroup's slice, one wave each at a time
     const int64_t mpad = (a.m + 15) / 16 * 16;
@@ -266,10 +285,10 @@ __device__ __forceinline__ void panel_body(const LinearArgs &a, const GeluArg *e
             const int lc = c * kTileN + 4 * (lane >> 4);
             const float4 sw = *reinterpret_cast<const float4 *>(vec + lc);
             const float4 bb = *reinterpret_cast<const float4 *>(vec + NT * kTileN + lc);
-            s[0] = a.sx * sw.x;
-            s[1] = a.sx * sw.y;
-            s[2] = a.sx * sw.z;
-            s[3] = a.sx * sw.w;
+            s[0] = sw.x;
+            s[1] = sw.y;
+            s[2] = sw.z;
+            s[3] = sw.w;
             bb4[0] = bb.x;
             bb4[1] = bb.y;
             bb4[2] = bb.z;
@@ -283,7 +302,37 @@ __device__ __forceinline__ void panel_body(const LinearArgs &a, const GeluArg *e
         // written too
         const int64_t mlim = YT ? mpad : a.m;
         const bool whole = t0 + S::TG <= mlim && (tile0 + NT) * kTileN <= a.n;
-        if constexpr (panel_transposes<KIND, YT, NT>()) {
+        if constexpr (EpiOut<KIND>::kBytes == 1 && YT && panel_transposes<KIND, YT, NT>()) {
+            if (whole && tile0 % 2 == 0) {
+                // int8 codes in the block layout: a lane holds 4 channels of
+                // one token, half of a 32-byte block row; each pair of tiles
+                // fills one 512-byte block (16 tokens x 32 channels), which
+                // goes through this wave's LDS area so that the store writes
+                // the whole block, 8 contiguous bytes a lane
+                uint32_t *const tr = reinterpret_cast<uint32_t *>(trans);
+                const int wi = (lane & 15) * 8 + (lane >> 4);  // word: token l%16, channels 4(l/16)..
+                int8_t *const y8 = static_cast<int8_t *>(a.y);
+#pragma unroll
+                for (int c = 0; c < NT; c += 2) {
+                    float s0[4], b0[4], s1[4], b1[4];
+                    scales(c, s0, b0);
+                    scales(c + 1, s1, b1);
+#pragma unroll
+                    for (int st = 0; st < ST; ++st) {
+                        const uint32_t v0 = epilogue_value<KIND>(a, acc[c][st], s0, b0, tab, hinv, eoff, cmax);
+                        const uint32_t v1 = epilogue_value<KIND>(a, acc[c + 1][st], s1, b1, tab, hinv, eoff, cmax);
+                        // (a wave's LDS operations take effect in order: the
+                        // previous block's read is done before these writes)
+                        tr[wi] = v0;
+                        tr[wi + 4] = v1;
+                        const uint2 r = *reinterpret_cast<const uint2 *>(tr + 2 * lane);
+                        int8_t *const p = y8 + t16x32_offset(t0 + st * 16, (tile0 + c) * kTileN, a.y_cb) + 8 * lane;
+                        *reinterpret_cast<uint2 *>(p) = r;
+                    }
+                }
+                return;
+            }
+        } else if constexpr (panel_transposes<KIND, YT, NT>()) {
             if (whole) {
                 // a lane's 16 bytes sit in a different row from its quad
                 // neighbours', so each pair of tiles goes through this wave's
@@ -388,12 +437,19 @@ __device__ __forceinline__ void panel_body(const LinearArgs &a, const GeluArg *e
         base = __builtin_amdgcn_readfirstlane(e.z) * 16u;
     };
     uint32_t cmask = 0, cbase = 0;  // the element being multiplied
+    // every wave issues the same R - 1 windows of row loads (zeros when it
+    // has no group), so that waiting until no more than that many loads are
+    // outstanding means its panel copies have landed; then a bare barrier
+    // (a full __syncthreads would also wait for the row loads)
+    row_offsets(n_my > 0 ? group_t0(0) : slice0, ro);
+    static_for<R - 1>([&](auto uc) {
+        constexpr int U = decltype(uc)::value;
+        load_rows(bv[U], ro, U < a.n_win ? phys(U) : 0, n_my > 0 && U < a.n_win);
+    });
+    wait_vmcnt_le<(R - 1) * ST * 2>();
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
     if (n_my > 0) {
-        row_offsets(group_t0(0), ro);
-        static_for<R - 1>([&](auto uc) {
-            constexpr int U = decltype(uc)::value;
-            load_rows(bv[U], ro, U < a.n_win ? phys(U) : 0, U < a.n_win);
-        });
         entry(0, cmask, cbase);
         read_main(ops[0], cbase);
         read_ovf(ops[0], cbase, cmask);

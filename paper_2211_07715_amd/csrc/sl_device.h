@@ -137,7 +137,8 @@ struct EpiOut<SL_EPI_F32_GELU> {
 };
 
 // Epilogue of one accumulator group: s = input scale x weight scales, b =
-// biases of the 4 channels; tab, hinv, off, cmax: the GELU step table.
+// biases of the 4 channels; tab, hinv, off, cmax (= kGeluBase + cells - 1):
+// the GELU step table.
 template <int KIND>
 __device__ __forceinline__ typename EpiOut<KIND>::T epilogue_value(const LinearArgs &a, const i32x4 acc,
                                                                    const float s[4], const float b[4],
@@ -153,9 +154,11 @@ __device__ __forceinline__ typename EpiOut<KIND>::T epilogue_value(const LinearA
         for (int r = 0; r < 4; ++r) {
             float y = (float)acc[r] * s[r];
             y = y + b[r];
-            const float c = __builtin_amdgcn_fmed3f(__builtin_fmaf(y, hinv, off), 0.0f, cmax);
-            // one 8-byte read: threshold, then the two codes
-            const uint2 cell = *reinterpret_cast<const uint2 *>(tab + (int)c);
+            const float c = __builtin_amdgcn_fmed3f(__builtin_fmaf(y, hinv, off), kGeluBase, cmax);
+            // one 8-byte read: threshold, then the two codes (the cell index
+            // is the low bits of c, see kGeluBase)
+            const uint32_t ci = __float_as_uint(c) - __float_as_uint(kGeluBase);
+            const uint2 cell = *reinterpret_cast<const uint2 *>(reinterpret_cast<const char *>(tab) + ci * 8u);
             const uint32_t q = y >= __uint_as_float(cell.x) ? cell.y >> 8 : cell.y;
             packed |= (q & 0xffu) << (8 * r);
         }

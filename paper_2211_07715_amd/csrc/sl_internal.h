@@ -58,8 +58,14 @@ struct alignas(8) GeluCell {
     int8_t q_hi;   // code from thr on
     int16_t pad;
 };
+// The cell of y is read off the bits of one fused multiply-add: off carries
+// kGeluBase = 1.5 * 2^23, where consecutive fp32 values are consecutive
+// integers, so t = med3(fma(y, hinv, off), kGeluBase, kGeluBase + nc - 1)
+// is kGeluBase plus the cell index (the fma rounds to nearest even), and the
+// index is bits(t) - bits(kGeluBase): no float-to-int conversion.
+constexpr float kGeluBase = 12582912.0f;
 struct GeluTable {
-    float hinv = 0, off = 0;  // cell(y) = clamp(trunc(fma(y, hinv, off)), 0, nc - 1)
+    float hinv = 0, off = 0;  // cell(y) = med3(fma(y, hinv, off), kGeluBase, kGeluBase + nc - 1) - kGeluBase
     int32_t nc = 0;
     bool ok = false;          // false: a cell would hold two changes; use erf
     GeluCell cell[kGeluCells];
