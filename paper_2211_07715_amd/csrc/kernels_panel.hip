@@ -548,9 +548,7 @@ static sl_status launch_panel_cfg(const LinearArgs &a, const GeluArg *ep, size_t
 // The compiled shapes: F(NT, ST, NWV, R).
 #define SL_PANEL_SHAPES(F) \
     F(6, 2, 8, 2)          \
-    F(6, 2, 4, 2)          \
     F(4, 2, 8, 2)          \
-    F(4, 4, 4, 2)          \
     F(2, 2, 8, 4)          \
     F(2, 4, 4, 2)
 

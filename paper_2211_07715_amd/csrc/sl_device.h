@@ -288,7 +288,7 @@ struct PanelCfg {
     int nt, st, nwv, r;
     int tg() const { return 16 * st; }
 };
-constexpr int kNumPanelCfgs = 6;
+constexpr int kNumPanelCfgs = 4;
 extern const PanelCfg kPanelCfgs[kNumPanelCfgs];
 // LDS bytes of a panel kernel launch holding `pieces` 16-byte panel pieces
 size_t panel_lds_bytes(PanelCfg c, int32_t run_kind, bool yt, int32_t n_win, int32_t pieces);
