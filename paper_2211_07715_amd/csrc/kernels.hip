@@ -560,7 +560,7 @@ __global__ __launch_bounds__(256) void quantize_vec16_kernel(const float *x, int
         o.y = quant4(src[1], inv);
         o.z = quant4(src[2], inv);
         o.w = quant4(src[3], inv);
-        reinterpret_cast<uint4 *>(q)[i] = o;
+        store_nt(reinterpret_cast<uint4 *>(q) + i, o);
     }
 }
 
@@ -602,7 +602,7 @@ __global__ __launch_bounds__(256) void quantize_t16x32_kernel(const float *x, in
                 o = make_uint4(v[0], v[1], v[2], v[3]);
             }
         }
-        reinterpret_cast<uint4 *>(q)[j] = o;
+        store_nt(reinterpret_cast<uint4 *>(q) + j, o);
     }
 }
 

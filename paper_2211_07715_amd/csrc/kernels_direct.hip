@@ -380,8 +380,8 @@ __device__ __forceinline__ void direct_body(const LinearArgs &a, const GeluArg *
                         const i32x4 r1 = *reinterpret_cast<const i32x4 *>(tr + ri + 8 * S::TRW);
                         const int64_t row = t0 + st * 16 + (lane >> 3);
                         int8_t *const p = y8 + (row * a.n + (tile0 + c) * kTileN + 4 * (lane & 7)) * 4;
-                        *reinterpret_cast<i32x4 *>(p) = r0;
-                        *reinterpret_cast<i32x4 *>(p + (int64_t)8 * a.n * 4) = r1;
+                        store_nt(p, r0);
+                        store_nt(p + (int64_t)8 * a.n * 4, r1);
                     }
                 }
                 return;
@@ -389,7 +389,6 @@ __device__ __forceinline__ void direct_body(const LinearArgs &a, const GeluArg *
         }
         if (t0 + ST * 16 <= mlim && (tile0 + NT) * kTileN <= a.n) {
             // whole tile: a uniform base and a lane offset, no bounds checks
-            using T = typename EpiOut<KIND>::T;
             constexpr int EB = EpiOut<KIND>::kBytes;
             int8_t *const y8 = static_cast<int8_t *>(a.y);
             const uint32_t lo = YT ? (uint32_t)(32 * (lane & 15) + 4 * (lane >> 4))
@@ -403,8 +402,7 @@ __device__ __forceinline__ void direct_body(const LinearArgs &a, const GeluArg *
                     const int32_t ch = (tile0 + c) * kTileN;
                     const int64_t uo = YT ? t16x32_offset(t0 + st * 16, ch, a.y_cb)
                                           : ((t0 + st * 16) * a.n + ch) * EB;
-                    *reinterpret_cast<T *>(y8 + uo + lo) =
-                        epilogue_value<KIND>(a, acc[c][st], s, bb4, tab, hinv, eoff, cmax);
+                    store_nt(y8 + uo + lo, epilogue_value<KIND>(a, acc[c][st], s, bb4, tab, hinv, eoff, cmax));
                 }
             }
         } else {

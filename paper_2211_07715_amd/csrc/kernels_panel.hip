@@ -327,7 +327,7 @@ __device__ __forceinline__ void panel_body(const LinearArgs &a, const GeluArg *e
                         tr[wi + 4] = v1;
                         const uint2 r = *reinterpret_cast<const uint2 *>(tr + 2 * lane);
                         int8_t *const p = y8 + t16x32_offset(t0 + st * 16, (tile0 + c) * kTileN, a.y_cb) + 8 * lane;
-                        *reinterpret_cast<uint2 *>(p) = r;
+                        store_nt(p, i32x2{(int)r.x, (int)r.y});
                     }
                 }
                 return;
@@ -361,8 +361,8 @@ __device__ __forceinline__ void panel_body(const LinearArgs &a, const GeluArg *e
                         const i32x4 r1 = *reinterpret_cast<const i32x4 *>(tr + ri + 8 * S::TRW);
                         const int64_t row = t0 + st * 16 + (lane >> 3);
                         int8_t *const p = y8 + (row * a.n + (tile0 + c) * kTileN + 4 * (lane & 7)) * 4;
-                        *reinterpret_cast<i32x4 *>(p) = r0;
-                        *reinterpret_cast<i32x4 *>(p + (int64_t)8 * a.n * 4) = r1;
+                        store_nt(p, r0);
+                        store_nt(p + (int64_t)8 * a.n * 4, r1);
                     }
                 }
                 return;
@@ -370,7 +370,6 @@ __device__ __forceinline__ void panel_body(const LinearArgs &a, const GeluArg *e
         }
         if (whole) {
             // whole group: a uniform base and a lane offset, no bounds checks
-            using T = typename EpiOut<KIND>::T;
             constexpr int EB = EpiOut<KIND>::kBytes;
             int8_t *const y8 = static_cast<int8_t *>(a.y);
             const uint32_t lo = YT ? (uint32_t)(32 * (lane & 15) + 4 * (lane >> 4))
@@ -384,8 +383,7 @@ __device__ __forceinline__ void panel_body(const LinearArgs &a, const GeluArg *e
                     const int32_t ch = (tile0 + c) * kTileN;
                     const int64_t uo =
                         YT ? t16x32_offset(t0 + st * 16, ch, a.y_cb) : ((t0 + st * 16) * a.n + ch) * EB;
-                    *reinterpret_cast<T *>(y8 + uo + lo) =
-                        epilogue_value<KIND>(a, acc[c][st], s, bb4, tab, hinv, eoff, cmax);
+                    store_nt(y8 + uo + lo, epilogue_value<KIND>(a, acc[c][st], s, bb4, tab, hinv, eoff, cmax));
                 }
             }
         } else {

@@ -12,8 +12,24 @@
 
 namespace sl {
 
+typedef int i32x2 __attribute__((ext_vector_type(2)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x8 __attribute__((ext_vector_type(8)));
+
+// Output store marked non-temporal: a kernel's outputs are read by a later
+// kernel, never by itself, so they need not displace its inputs in the caches.
+template <class V>
+__device__ __forceinline__ void store_nt(void *p, V v)
+{
+    if constexpr (sizeof(V) == 4) {
+        __builtin_nontemporal_store(__builtin_bit_cast(uint32_t, v), reinterpret_cast<uint32_t *>(p));
+    } else if constexpr (sizeof(V) == 8) {
+        __builtin_nontemporal_store(__builtin_bit_cast(i32x2, v), reinterpret_cast<i32x2 *>(p));
+    } else {
+        static_assert(sizeof(V) == 16, "4, 8 or 16-byte stores");
+        __builtin_nontemporal_store(__builtin_bit_cast(i32x4, v), reinterpret_cast<i32x4 *>(p));
+    }
+}
 
 constexpr int kXcds = 8;  // accelerator complex dies, each with its own L2
 constexpr int kMaxDevices = 64;
@@ -191,10 +207,9 @@ __device__ __forceinline__ void epilogue_store(const LinearArgs &a, const i32x4 
                                                float hinv, float off, float cmax)
 {
     if (tok >= a.m) return;
-    using T = typename EpiOut<KIND>::T;
     static_assert(!YT || EpiOut<KIND>::kBytes == 1, "the block layout holds int8 outputs");
     const int64_t o = YT ? t16x32_offset(tok, ch0, a.y_cb) : (tok * a.n + ch0) * EpiOut<KIND>::kBytes;
-    *reinterpret_cast<T *>(static_cast<int8_t *>(a.y) + o) = epilogue_value<KIND>(a, acc, s, b, tab, hinv, off, cmax);
+    store_nt(static_cast<int8_t *>(a.y) + o, epilogue_value<KIND>(a, acc, s, b, tab, hinv, off, cmax));
 }
 
 typedef __attribute__((address_space(3))) void lds_void;
