@@ -1073,7 +1073,8 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int32_t x_la
         const bool vec = xt || ((w->k_in % 16 == 0) && ((reinterpret_cast<uintptr_t>(a.x) & 15) == 0));
         // Aligned or block-layout rows: the weight-stationary kernel where it
         // pays (its 96-channel panel fits in LDS and every wave of a
-        // workgroup gets at least two token groups, evenly), else the
+        // workgroup gets at least eight token groups, or at least two, evenly,
+        // with at most three overflow operands per four main ones), else the
         // direct-operand kernel (block-layout input, or block-layout output
         // from aligned rows) or the staged kernel (row-major input and
         // output). SL_PATH=panel|direct|staged forces a kernel (tests,
@@ -1085,9 +1086,16 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int32_t x_la
             PanelCfg pc{};
             size_t lds = 0;
             sl_status pst = choose_panel_cfg(a, w, run_kind, yt, &pc, &lds, force_panel ? nullptr : &kPanelDefault);
-            if (pst == SL_OK && !force_panel &&
-                !(a.slice_groups >= 2 * pc.nwv && (a.slice_groups % pc.nwv == 0 || a.slice_groups >= 8 * pc.nwv)))
-                pst = SL_ERR_UNSUPPORTED;
+            if (pst == SL_OK && !force_panel) {
+                // overflow operands per main operand in the largest panel
+                int32_t pieces = 0;
+                for (int i = 0; i < w->dev.n_pan; ++i)
+                    if (w->dev.pan_nt[i] == pc.nt) pieces = w->dev.pan_pieces[i];
+                const double ovf = (double)pieces / ((double)ti.n_win * pc.nt * kOpPieces) - 1.0;
+                const bool long_slices = a.slice_groups >= 8 * pc.nwv;
+                const bool even_slices = a.slice_groups >= 2 * pc.nwv && a.slice_groups % pc.nwv == 0;
+                if (!(long_slices || (even_slices && ovf <= 0.75))) pst = SL_ERR_UNSUPPORTED;
+            }
             if (pst == SL_OK) {
                 pst = launch_panel(a, run_kind == SL_EPI_I8_GELU ? &ga : nullptr, run_kind, pc, xt, yt, lds, s);
                 if (pst != SL_OK) return pst;

@@ -104,22 +104,25 @@ def test_panel_runs_at_distilbert_ffn_shapes(hip, monkeypatch):
 
 def test_default_path_choice(hip, monkeypatch):
     """Without SL_PATH the weight-stationary kernel runs where every wave gets
-    at least two token groups (DistilBERT FFN1 at 4096 tokens) and the other
-    kernels run where its panel does not fit (FFN2) or the tokens are few."""
+    enough token groups for the panel's density (DistilBERT FFN1 at 90 % and
+    4096 tokens, at 80 % from 16384 tokens) and the other kernels run where
+    its panel does not fit (FFN2), overflows are dense for few tokens (FFN1
+    at 80 % and 4096 tokens) or the tokens are few."""
     import torch
     import workloads as wk
     monkeypatch.delenv("SL_PATH", raising=False)
     monkeypatch.delenv("SL_PTILE", raising=False)
-    for (n, k, m, want) in [(3072, 768, 4096, "panel 6,2,8,2"), (768, 3072, 4096, "direct"),
-                            (768, 768, 128, "direct")]:
-        wd = wk.make_weight(n, k, 0.9, seed=3)
+    for (n, k, m, s, want) in [(3072, 768, 4096, 0.9, "panel 6,2,8,2"), (3072, 768, 4096, 0.8, "direct"),
+                               (3072, 768, 16384, 0.8, "panel 6,2,8,2"), (768, 3072, 4096, 0.9, "direct"),
+                               (768, 768, 128, 0.9, "direct")]:
+        wd = wk.make_weight(n, k, s, seed=3)
         x = wk.make_x(m, k, seed=3)
         pw = hip.PackedWeight.pack(wd["w"], wd["sw"], wd["b"])
         xb = torch.from_numpy(np.ascontiguousarray(hip.to_t16x32(x))).cuda()
         y = pw.run(xb, 0.02, KINDS["acc_i32"], x_layout=T, m_tokens=m)
         torch.cuda.synchronize()
         path = hip.last_path()
-        say(f"default {n}x{k} m={m}: {path}")
+        say(f"default {n}x{k} s={s} m={m}: {path}")
         assert path.startswith(want), path
         rows = np.arange(0, m, max(1, m // 48))
         check(0, y.cpu().numpy()[rows], oracle.acc(np.ascontiguousarray(x[rows]), wd["w"]), f"{n}x{k} m={m}")
