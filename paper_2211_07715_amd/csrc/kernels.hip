@@ -1037,6 +1037,7 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int32_t x_la
     a.inv_so = inv_so;
     a.n_tiles = ti.n_tiles;
     a.n_win = ti.n_win;
+    a.om = nullptr;
     a.pan = nullptr;
     a.img_bytes = 0;
     a.ovf_off = 0;
