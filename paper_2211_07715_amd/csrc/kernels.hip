@@ -708,6 +708,38 @@ sl_status upload_image(sl_packed_weight *w)
             pan_max[i] = (uint32_t)std::min<uint64_t>(std::max<uint64_t>(pan_max[i], base), UINT32_MAX);
         }
     }
+    // The panel images: per channel group, its window table and then its
+    // panel (per window: the NT main operands, zeros past the last tile, then
+    // the window's overflow operands), padded to a common stride of whole
+    // 1024-byte copies, so that a workgroup's copies need no table read first.
+    // Only sizes whose panels can fit in LDS get an image.
+    std::vector<std::vector<int8_t>> pimgs(pnts.size());
+    std::vector<uint32_t> pstrides(pnts.size(), 0);
+    for (size_t i = 0; i < pnts.size(); ++i) {
+        const int nt = pnts[i];
+        const int ncg = (ti.n_tiles + nt - 1) / nt;
+        const uint64_t tab = (uint64_t)(ti.n_win + 1) * 16;
+        const uint64_t stride = (tab + (uint64_t)pan_max[i] * 16 + 1023) / 1024 * 1024;
+        if (stride > kLdsMax || (uint64_t)ncg * stride > (uint64_t)kMaxBufferBytes) continue;
+        pstrides[i] = (uint32_t)stride;
+        std::vector<int8_t> &im = pimgs[i];
+        im.assign((size_t)ncg * stride, 0);
+        const std::vector<uint32_t> &pt = pans[i];
+        for (int g = 0; g < ncg; ++g) {
+            int8_t *const gb = im.data() + (size_t)g * stride;
+            const uint32_t *const ge = pt.data() + (size_t)g * (ti.n_win + 1) * 4;
+            memcpy(gb, ge, (size_t)tab);
+            const int t0 = g * nt, ntl = std::min(nt, ti.n_tiles - t0);
+            for (int wi = 0; wi < ti.n_win; ++wi) {
+                int8_t *const wb = gb + tab + (size_t)ge[wi * 4 + 2] * 16;
+                memcpy(wb, ti.main.data() + ((size_t)wi * ti.n_tiles + t0) * kOpBytes, (size_t)ntl * kOpBytes);
+                const uint32_t n_ovf = (uint32_t)__builtin_popcount(ge[wi * 4]);
+                if (n_ovf)
+                    memcpy(wb + (size_t)nt * kOpBytes, ti.ovf.data() + (size_t)ge[wi * 4 + 1] * kOpBytes,
+                                (size_t)n_ovf * kOpBytes);
+            }
+        }
+    }
     const size_t b_main = std::max<size_t>(ti.main.size(), 16);
     const size_t b_ovf = std::max<size_t>(ti.ovf.size(), 16);
     const size_t b_vec = (size_t)w->n_out * sizeof(float);
@@ -724,7 +756,7 @@ sl_status upload_image(sl_packed_weight *w)
     std::vector<size_t> o_pan(pnts.size());
     for (size_t i = 0; i < pnts.size(); ++i) {
         o_pan[i] = o_end;
-        o_end = align256(o_end + pans[i].size() * sizeof(uint32_t));
+        o_end = align256(o_end + pimgs[i].size());
     }
     const size_t total = o_end;
     void *base = nullptr;
@@ -748,14 +780,14 @@ sl_status upload_image(sl_packed_weight *w)
     }
     w->dev.n_om = (int32_t)nts.size();
     for (size_t i = 0; i < pnts.size(); ++i) {
-        HIP_TRY(hipMemcpy(p + o_pan[i], pans[i].data(), pans[i].size() * sizeof(uint32_t), hipMemcpyHostToDevice));
+        if (!pimgs[i].empty())
+            HIP_TRY(hipMemcpy(p + o_pan[i], pimgs[i].data(), pimgs[i].size(), hipMemcpyHostToDevice));
         w->dev.pan_nt[i] = pnts[i];
         w->dev.pan_pieces[i] = (int32_t)std::min<uint32_t>(pan_max[i], INT32_MAX);
-        w->dev.pan[i] = reinterpret_cast<const uint32_t *>(p + o_pan[i]);
+        w->dev.pan_stride[i] = pstrides[i];
+        w->dev.pan[i] = pimgs[i].empty() ? nullptr : reinterpret_cast<const int8_t *>(p + o_pan[i]);
     }
     w->dev.n_pan = (int32_t)pnts.size();
-    w->dev.img_bytes = (uint32_t)(o_ovf + ti.ovf.size());
-    w->dev.ovf_off = (uint32_t)o_ovf;
     w->dev.main = reinterpret_cast<const int8_t *>(p + o_main);
     w->dev.ovf = reinterpret_cast<const int8_t *>(p + o_ovf);
     w->dev.ovf_ptr = nullptr;
@@ -961,9 +993,9 @@ static sl_status choose_panel_cfg(LinearArgs &a, const sl_packed_weight *w, int3
         int pi = -1;
         for (int i = 0; i < w->dev.n_pan; ++i)
             if (w->dev.pan_nt[i] == c.nt) pi = i;
-        if (pi < 0) continue;
+        if (pi < 0 || !w->dev.pan_stride[pi]) continue;
         const int32_t pieces = w->dev.pan_pieces[pi];
-        const size_t lds = panel_lds_bytes(c, run_kind, yt, w->tiles.n_win, pieces);
+        const size_t lds = panel_lds_bytes(c, run_kind, yt, w->dev.pan_stride[pi]);
         if (lds > kLdsMax) continue;
         // resident workgroups per device, cached per (device, shape, LDS size)
         static thread_local struct {
@@ -1005,11 +1037,11 @@ static sl_status choose_panel_cfg(LinearArgs &a, const sl_packed_weight *w, int3
             a.n_slices = (int32_t)n_sl;
             a.slice_groups = (int32_t)sg;
             a.pan = w->dev.pan[pi];
+            a.pan_bytes = (uint32_t)(n_cg * w->dev.pan_stride[pi]);
+            a.pan_instr = (int32_t)(w->dev.pan_stride[pi] / 1024);
         }
     }
     if (!found) return SL_ERR_UNSUPPORTED;
-    a.img_bytes = w->dev.img_bytes;
-    a.ovf_off = w->dev.ovf_off;
     return SL_OK;
 }
 
@@ -1039,8 +1071,8 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int32_t x_la
     a.n_win = ti.n_win;
     a.om = nullptr;
     a.pan = nullptr;
-    a.img_bytes = 0;
-    a.ovf_off = 0;
+    a.pan_bytes = 0;
+    a.pan_instr = 0;
     a.n_slices = 0;
     a.slice_groups = 0;
     hipStream_t s = static_cast<hipStream_t>(stream);

@@ -8,9 +8,10 @@
 // column indices select the input columns the block mask names, int32
 // accumulation, one fused epilogue per output after the whole reduction).
 // What differs is the schedule. A workgroup owns one channel group (NT
-// 16-channel tiles) and one slice of the tokens. It copies the group's whole
-// panel -- every window's NT main operands and the overflow operands the
-// window holds, packed -- from the image into LDS once, then its waves work
+// 16-channel tiles) and one slice of the tokens. It copies the group's window
+// table and whole panel -- every window's NT main operands and the overflow
+// operands the window holds, packed, laid out that way by the packer -- into
+// LDS once, with no dependent read before the copies, then its waves work
 // through the slice's token groups on their own: a wave loads its token rows
 // (the B operands) straight into registers, R - 1 windows ahead, reads the weight
 // operands from the resident panel, and multiplies an overflow operand only
@@ -50,18 +51,16 @@ constexpr bool panel_transposes()
 }
 
 // LDS layout: weight scales and biases | GELU step table | per-wave transpose
-// areas | window table (n_win + 1 entries of 16 bytes) | panel
+// areas | window table (n_win + 1 entries of 16 bytes) and panel, as one
+// stride of the panel image
 template <int KIND, int NT, int ST, int NWV, bool YT>
 struct PLds {
     using S = PShape<NT, ST, NWV>;
     static constexpr int kTab = KIND == SL_EPI_I8_GELU ? kGeluLds : 0;
     static constexpr int kTr = panel_transposes<KIND, YT, NT>() ? NWV * S::TR : 0;
     static constexpr int kFixed = S::VEC + kTab + kTr;
-    static size_t bytes(int32_t n_win, int32_t pieces)
-    {
-        // the copy runs in whole 64-piece instructions
-        return (size_t)kFixed + (size_t)(n_win + 1) * 16 + (size_t)(pieces + 63) / 64 * 1024;
-    }
+    static_assert(kFixed % 16 == 0, "the copies write 16-byte pieces");
+    static size_t bytes(uint32_t stride) { return (size_t)kFixed + stride; }
 };
 
 // Calls f(std::integral_constant<int, 0>) .. f(std::integral_constant<int, N-1>) in order.
@@ -102,73 +101,27 @@ __device__ __forceinline__ void panel_body(const LinearArgs &a, const GeluArg *e
     uint4 *const wtab = reinterpret_cast<uint4 *>(smem + L::kFixed);
     int8_t *const panel = smem + L::kFixed + (a.n_win + 1) * 16;
 
-    // ---- set-up: window table, scales and biases, GELU table
-    const uint4 *const pt = reinterpret_cast<const uint4 *>(a.pan) + (size_t)cg * (a.n_win + 1);
-    for (int w = tid; w <= a.n_win; w += S::NTH) wtab[w] = pt[w];
-    if constexpr (KIND != SL_EPI_ACC_I32) {
-        for (int i = tid; i < NT * kTileN; i += S::NTH) {
-            const int32_t ch = tile0 * kTileN + i;
-            // the dequantisation scale sx * sw[n], one fp32 product as in the definition
-            vec[i] = ch < a.n ? a.sx * a.w_scale[ch] : 0.0f;
-            vec[NT * kTileN + i] = ch < a.n ? a.bias[ch] : 0.0f;
-        }
-    }
-    float hinv = 0.0f, eoff = 0.0f, cmax = 0.0f;
-    if constexpr (KIND == SL_EPI_I8_GELU) {
-        for (int u = tid; u < ep->nc; u += S::NTH) tab[u] = ep->cell[u];
-        hinv = ep->hinv;
-        eoff = ep->off;
-        cmax = kGeluBase + (float)(ep->nc - 1);
-    }
-    __syncthreads();
-
-    // ---- the panel: 16-byte piece p of the group's panel comes from window
-    // w with base(w) <= p < base(w+1): main operand pieces of tiles tile0 ..
-    // (zeros past the last tile), then the window's overflow operands. Copy
-    // instruction j of the workgroup moves pieces 64j .. 64j+63 (global to
-    // LDS, no registers); wave v issues instructions v, v + NWV, ... All
-    // source offsets are worked out first: an LDS read between the copies
-    // would make each copy wait for the ones before it.
+    // ---- the group's window table and panel: one stride of the panel image,
+    // copied global to LDS (no registers) in 1024-byte instructions, wave v
+    // issuing instructions v, v + NWV, ...; nothing is read before them, so
+    // the copies start at once and land while the set-up runs
     {
         constexpr int kMaxCopies = (int)((kLdsMax / 1024 + NWV - 1) / NWV);
         const __amdgpu_buffer_rsrc_t ir =
-            __builtin_amdgcn_make_buffer_rsrc((void *)a.main, 0, (int)a.img_bytes, kRsrcWord3);
-        const uint32_t total = wtab[a.n_win].z;
-        const int n_instr = (int)((total + 63) / 64);
-        uint32_t offs[kMaxCopies];
-        int cw = 0;  // this lane's window cursor: pieces only grow
+            __builtin_amdgcn_make_buffer_rsrc((void *)a.pan, 0, (int)a.pan_bytes, kRsrcWord3);
+        const uint32_t src = (uint32_t)cg * (uint32_t)a.pan_instr * 1024u + (uint32_t)lane * 16u;
+        int8_t *const dst = smem + L::kFixed;
 #pragma unroll
         for (int i = 0; i < kMaxCopies; ++i) {
             const int j = wave + i * NWV;
-            uint32_t off = kOob;
-            if (j < n_instr) {
-                const uint32_t p = (uint32_t)j * 64 + (uint32_t)lane;
-                while (cw + 1 < a.n_win && p >= wtab[cw + 1].z) ++cw;
-                const uint4 e = wtab[cw];
-                const uint32_t q = p - e.z;
-                if (p < total) {
-                    if (q < (uint32_t)(NT * kOpPieces)) {
-                        const uint32_t t = q / kOpPieces;
-                        if (tile0 + (int32_t)t < a.n_tiles)
-                            off = ((uint32_t)(cw * a.n_tiles + tile0) * kOpPieces + q) * 16u;
-                    } else {
-                        off = a.ovf_off + (e.y * kOpPieces + (q - NT * kOpPieces)) * 16u;
-                    }
-                }
-            }
-            offs[i] = off;
-        }
-#pragma unroll
-        for (int i = 0; i < kMaxCopies; ++i) {
-            const int j = wave + i * NWV;
-            if (j < n_instr)
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(ir, (lds_void *)(panel + (size_t)j * 1024), 16, offs[i], 0,
-                                                         0, 0);
+            if (j < a.pan_instr)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(ir, (lds_void *)(dst + (size_t)j * 1024), 16,
+                                                         src + (uint32_t)j * 1024u, 0, 0, 0);
         }
     }
-    // (the first token rows load while the panel copies are in flight; the
-    // wait for the copies comes after them)
-    asm volatile("" ::: "memory");
+
+    float hinv = 0.0f, eoff = 0.0f, cmax = 0.0f;  // GELU table parameters (set-up below)
+
 
     // ---- token groups of this workgroup's slice, one wave each at a time
     const int64_t mpad = (a.m + 15) / 16 * 16;
@@ -435,18 +388,33 @@ __device__ __forceinline__ void panel_body(const LinearArgs &a, const GeluArg *e
         base = __builtin_amdgcn_readfirstlane(e.z) * 16u;
     };
     uint32_t cmask = 0, cbase = 0;  // the element being multiplied
-    // every wave issues the same R - 1 windows of row loads (zeros when it
-    // has no group), so that waiting until no more than that many loads are
-    // outstanding means its panel copies have landed; then a bare barrier
-    // (a full __syncthreads would also wait for the row loads)
+    // the first R - 1 windows of token rows load while the panel copies are
+    // in flight, then the set-up; one barrier after all of them, past which
+    // table, panel, scales and GELU table are in LDS
     row_offsets(n_my > 0 ? group_t0(0) : slice0, ro);
     static_for<R - 1>([&](auto uc) {
         constexpr int U = decltype(uc)::value;
         load_rows(bv[U], ro, U < a.n_win ? phys(U) : 0, n_my > 0 && U < a.n_win);
     });
-    wait_vmcnt_le<(R - 1) * ST * 2>();
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
+    // ---- set-up: scales and biases, GELU table
+    static_assert(NT * kTileN <= S::NTH, "one scale and one bias a thread");
+    if constexpr (KIND != SL_EPI_ACC_I32) {
+        if (tid < NT * kTileN) {
+            const int32_t ch = tile0 * kTileN + tid;
+            // the dequantisation scale sx * sw[n], one fp32 product as in the definition
+            vec[tid] = ch < a.n ? a.sx * a.w_scale[ch] : 0.0f;
+            vec[NT * kTileN + tid] = ch < a.n ? a.bias[ch] : 0.0f;
+        }
+    }
+    if constexpr (KIND == SL_EPI_I8_GELU) {
+        for (int u = tid; u < ep->nc; u += S::NTH) tab[u] = ep->cell[u];
+        hinv = ep->hinv;
+        eoff = ep->off;
+        cmax = kGeluBase + (float)(ep->nc - 1);
+    }
+    // every wave's copies (and first token rows) have landed before the barrier
+    wait_vmcnt_le<0>();
+    __syncthreads();
     if (n_my > 0) {
         entry(0, cmask, cbase);
         read_main(ops[0], cbase);
@@ -570,26 +538,26 @@ static sl_status launch_panel_kind(const LinearArgs &a, const GeluArg *ep, Panel
 }
 
 template <int KIND>
-static size_t panel_lds_kind(PanelCfg c, bool yt, int32_t n_win, int32_t pieces)
+static size_t panel_lds_kind(PanelCfg c, bool yt, uint32_t stride)
 {
 #define SL_PANEL_LDS(NT_, ST_, NWV_, R_)                                                          \
     if (c.nt == NT_ && c.st == ST_ && c.nwv == NWV_ && c.r == R_)                                 \
-        return yt ? PLds<KIND, NT_, ST_, NWV_, true>::bytes(n_win, pieces)                        \
-                  : PLds<KIND, NT_, ST_, NWV_, false>::bytes(n_win, pieces);
+        return yt ? PLds<KIND, NT_, ST_, NWV_, true>::bytes(stride)                               \
+                  : PLds<KIND, NT_, ST_, NWV_, false>::bytes(stride);
     SL_PANEL_SHAPES(SL_PANEL_LDS)
 #undef SL_PANEL_LDS
     return (size_t)-1;
 }
 
-size_t panel_lds_bytes(PanelCfg c, int32_t run_kind, bool yt, int32_t n_win, int32_t pieces)
+size_t panel_lds_bytes(PanelCfg c, int32_t run_kind, bool yt, uint32_t stride)
 {
     switch (run_kind) {
-    case SL_EPI_ACC_I32: return panel_lds_kind<SL_EPI_ACC_I32>(c, false, n_win, pieces);
-    case SL_EPI_F32: return panel_lds_kind<SL_EPI_F32>(c, false, n_win, pieces);
-    case SL_EPI_F32_GELU: return panel_lds_kind<SL_EPI_F32_GELU>(c, false, n_win, pieces);
-    case SL_EPI_I8: return panel_lds_kind<SL_EPI_I8>(c, yt, n_win, pieces);
-    case SL_EPI_I8_GELU: return panel_lds_kind<SL_EPI_I8_GELU>(c, yt, n_win, pieces);
-    default: return panel_lds_kind<kEpiI8GeluErf>(c, yt, n_win, pieces);
+    case SL_EPI_ACC_I32: return panel_lds_kind<SL_EPI_ACC_I32>(c, false, stride);
+    case SL_EPI_F32: return panel_lds_kind<SL_EPI_F32>(c, false, stride);
+    case SL_EPI_F32_GELU: return panel_lds_kind<SL_EPI_F32_GELU>(c, false, stride);
+    case SL_EPI_I8: return panel_lds_kind<SL_EPI_I8>(c, yt, stride);
+    case SL_EPI_I8_GELU: return panel_lds_kind<SL_EPI_I8_GELU>(c, yt, stride);
+    default: return panel_lds_kind<kEpiI8GeluErf>(c, yt, stride);
     }
 }
 

@@ -74,9 +74,10 @@ struct LinearArgs {
     int32_t x_cb;       // 32-feature column blocks of x (SL_LAYOUT_T16X32 input)
     int32_t y_cb;       // 32-channel column blocks of y (SL_LAYOUT_T16X32 output)
     // weight-stationary kernel only
-    const uint32_t *pan;    // panel table of this launch's tile-group size, [n_cgroups][n_win + 1][4]
-    uint32_t img_bytes;     // main image through the end of the overflow operands
-    uint32_t ovf_off;       // byte offset of the overflow operands from main
+    const int8_t *pan;      // panel image of this launch's channel-group size: per group, its window
+                            // table ([n_win + 1][4] words) and panel, pan_instr KiB apart
+    uint32_t pan_bytes;     // bytes of that image (the range of the copies)
+    int32_t pan_instr;      // 1024-byte copies per channel group
     int32_t n_slices;       // token slices per channel group
     int32_t slice_groups;   // token groups (16 ST tokens) per slice
 };
@@ -305,8 +306,9 @@ struct PanelCfg {
 };
 constexpr int kNumPanelCfgs = 4;
 extern const PanelCfg kPanelCfgs[kNumPanelCfgs];
-// LDS bytes of a panel kernel launch holding `pieces` 16-byte panel pieces
-size_t panel_lds_bytes(PanelCfg c, int32_t run_kind, bool yt, int32_t n_win, int32_t pieces);
+// LDS bytes of a panel kernel launch whose channel groups' tables and panels
+// take `stride` bytes each
+size_t panel_lds_bytes(PanelCfg c, int32_t run_kind, bool yt, uint32_t stride);
 sl_status launch_panel(const LinearArgs &a, const GeluArg *ep, int32_t run_kind, PanelCfg c, bool xt, bool yt,
                        size_t lds, hipStream_t stream);
 // resident workgroups of a panel-kernel shape for `lds` bytes of LDS (all kinds and layouts of a

@@ -100,9 +100,13 @@ struct DeviceImage {
     int32_t n_pan = 0;
     int32_t pan_nt[kMaxPanTables] = {};
     int32_t pan_pieces[kMaxPanTables] = {};  // largest panel over the groups, 16-byte pieces
-    const uint32_t *pan[kMaxPanTables] = {};
-    uint32_t img_bytes = 0;  // main image through the end of the overflow operands
-    uint32_t ovf_off = 0;    // byte offset of the overflow operands from the main image
+    // per channel-group size: each group's window table ([n_win + 1][4]
+    // words: overflow mask, first overflow operand, panel offset in pieces)
+    // followed by its panel, byte for byte as the weight-stationary kernel
+    // holds them in LDS, groups pan_stride bytes apart (a multiple of 1024;
+    // 0: the panels do not fit in LDS and there is no such image)
+    uint32_t pan_stride[kMaxPanTables] = {};
+    const int8_t *pan[kMaxPanTables] = {};
     int64_t bytes = 0;
 };
 
