@@ -962,18 +962,17 @@ static DirectCfg choose_direct_cfg(int64_t m, const sl_packed_weight *w)
     return best ? *best : *most;
 }
 
-// The weight-stationary shape the default path uses: 96 channels x 32
-// tokens per wave, 8 waves.
-static const PanelCfg kPanelDefault{6, 2, 8, 2};
+// The default path takes the weight-stationary kernel only for reductions
+// of at most this many 128-feature windows (K <= 1024).
+constexpr int32_t kPanelMaxWin = 8;
 
 // Weight-stationary shape for a launch of a.m tokens: the compiled shapes
 // whose largest panel fits in LDS are scored by the bytes their workgroups
 // read (token rows once per channel group, the panel once per workgroup)
-// spread over the CUs they keep busy (only: consider that shape alone);
-// SL_PTILE="nt,st,nwv,r" overrides. Fills a's channel-group and slice
+// spread over the CUs they keep busy; SL_PTILE="nt,st,nwv,r" overrides. Fills a's channel-group and slice
 // fields; SL_ERR_UNSUPPORTED when no panel fits.
 static sl_status choose_panel_cfg(LinearArgs &a, const sl_packed_weight *w, int32_t run_kind, bool yt, PanelCfg *out,
-                                  size_t *lds_out, const PanelCfg *only)
+                                  size_t *lds_out)
 {
     int n_cu = 0, dev = 0;
     HIP_TRY(hipGetDevice(&dev));
@@ -989,7 +988,6 @@ static sl_status choose_panel_cfg(LinearArgs &a, const sl_packed_weight *w, int3
         const PanelCfg c = kPanelCfgs[ci];
         if (have_forced && (c.nt != forced.nt || c.st != forced.st || c.nwv != forced.nwv || c.r != forced.r))
             continue;
-        if (only && (c.nt != only->nt || c.st != only->st || c.nwv != only->nwv || c.r != only->r)) continue;
         int pi = -1;
         for (int i = 0; i < w->dev.n_pan; ++i)
             if (w->dev.pan_nt[i] == c.nt) pi = i;
@@ -1105,30 +1103,23 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int32_t x_la
         a.m = std::min(chunk, m - t0);
         const bool vec = xt || ((w->k_in % 16 == 0) && ((reinterpret_cast<uintptr_t>(a.x) & 15) == 0));
         // Aligned or block-layout rows: the weight-stationary kernel where it
-        // pays (its 96-channel panel fits in LDS and every wave of a
-        // workgroup gets at least eight token groups, or at least two, evenly,
-        // with at most three overflow operands per four main ones), else the
-        // direct-operand kernel (block-layout input, or block-layout output
-        // from aligned rows) or the staged kernel (row-major input and
-        // output). SL_PATH=panel|direct|staged forces a kernel (tests,
-        // tuning; panel falls back when no panel fits).
+        // pays -- a short reduction (at most kPanelMaxWin windows), and either
+        // a widening layer (N > K: many channel groups share each token row)
+        // or slices of at least four token groups per wave (the panel filled
+        // once is used for many tokens) -- with the shape the cost model
+        // picks; else the direct-operand kernel (block-layout input, or
+        // block-layout output from aligned rows) or the staged kernel
+        // (row-major input and output). SL_PATH=panel|direct|staged forces a
+        // kernel (tests, tuning; panel falls back when no panel fits).
         const char *path = getenv("SL_PATH");
         const bool force_panel = path && strcmp(path, "panel") == 0;
         const bool auto_path = !path || !*path;
-        if (vec && (force_panel || auto_path)) {
+        if (vec && (force_panel || (auto_path && ti.n_win <= kPanelMaxWin))) {
             PanelCfg pc{};
             size_t lds = 0;
-            sl_status pst = choose_panel_cfg(a, w, run_kind, yt, &pc, &lds, force_panel ? nullptr : &kPanelDefault);
-            if (pst == SL_OK && !force_panel) {
-                // overflow operands per main operand in the largest panel
-                int32_t pieces = 0;
-                for (int i = 0; i < w->dev.n_pan; ++i)
-                    if (w->dev.pan_nt[i] == pc.nt) pieces = w->dev.pan_pieces[i];
-                const double ovf = (double)pieces / ((double)ti.n_win * pc.nt * kOpPieces) - 1.0;
-                const bool long_slices = a.slice_groups >= 8 * pc.nwv;
-                const bool even_slices = a.slice_groups >= 2 * pc.nwv && a.slice_groups % pc.nwv == 0;
-                if (!(long_slices || (even_slices && ovf <= 0.75))) pst = SL_ERR_UNSUPPORTED;
-            }
+            sl_status pst = choose_panel_cfg(a, w, run_kind, yt, &pc, &lds);
+            if (pst == SL_OK && !force_panel && !(w->n_out > w->k_in || a.slice_groups >= 4 * pc.nwv))
+                pst = SL_ERR_UNSUPPORTED;
             if (pst == SL_OK) {
                 pst = launch_panel(a, run_kind == SL_EPI_I8_GELU ? &ga : nullptr, run_kind, pc, xt, yt, lds, s);
                 if (pst != SL_OK) return pst;

@@ -103,17 +103,17 @@ def test_panel_runs_at_distilbert_ffn_shapes(hip, monkeypatch):
 
 
 def test_default_path_choice(hip, monkeypatch):
-    """Without SL_PATH the weight-stationary kernel runs where every wave gets
-    enough token groups for the panel's density (DistilBERT FFN1 at 90 % and
-    4096 tokens, at 80 % from 16384 tokens) and the other kernels run where
-    its panel does not fit (FFN2), overflows are dense for few tokens (FFN1
-    at 80 % and 4096 tokens) or the tokens are few."""
+    """Without SL_PATH the weight-stationary kernel runs for short reductions
+    (K <= 1024) of widening layers (DistilBERT QKV and FFN1, any token count)
+    or of long token slices, and the direct kernel elsewhere: FFN2 (K = 3072)
+    and the square attention-output layer at few tokens."""
     import torch
     import workloads as wk
     monkeypatch.delenv("SL_PATH", raising=False)
     monkeypatch.delenv("SL_PTILE", raising=False)
-    for (n, k, m, s, want) in [(3072, 768, 4096, 0.9, "panel 6,2,8,2"), (3072, 768, 4096, 0.8, "direct"),
-                               (3072, 768, 16384, 0.8, "panel 6,2,8,2"), (768, 3072, 4096, 0.9, "direct"),
+    for (n, k, m, s, want) in [(3072, 768, 4096, 0.9, "panel 6,2,8,2"), (3072, 768, 4096, 0.8, "panel 6,2,8,2"),
+                               (3072, 768, 16384, 0.8, "panel 6,2,8,2"), (2304, 768, 384, 0.8, "panel"),
+                               (768, 3072, 4096, 0.9, "direct"), (768, 768, 4096, 0.8, "direct"),
                                (768, 768, 128, 0.9, "direct")]:
         wd = wk.make_weight(n, k, s, seed=3)
         x = wk.make_x(m, k, seed=3)
