@@ -221,9 +221,11 @@ int32_t sl_abi_version(void);
 /*
  * Thread-local text naming the kernel and workgroup shape of the last
  * successful sparse_linear_run / sparse_linear_run_layout on this thread
- * ("" before the first): "panel nt,st,nwv" (weight-stationary), "direct
- * st,nt,wm,d" or "staged st,ct,wm,wn,d". For tests and tuning; the text is
- * valid until the next run on this thread.
+ * ("" before the first): "panel nt,st,nwv,r" (weight-stationary), "direct
+ * st,nt,wm,d" or "staged st,ct,wm,wn,d", followed by " gelu=erf" when an
+ * int8 GELU epilogue evaluated erf because its output scale (below about
+ * 0.015) admits no step table. For tests and tuning; the text is valid until
+ * the next run on this thread.
  */
 const char *sl_last_path(void);
 

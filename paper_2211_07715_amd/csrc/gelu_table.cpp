@@ -10,8 +10,8 @@
 // (the same operations, in the same order, as the definition). The kernel
 // then needs one compare per output instead of an erf evaluation.
 //
-// A table whose cells would hold more than one change (very small output
-// scales) is reported as unusable and the kernel evaluates erf instead.
+// A table whose cells would hold more than one change (output scales below
+// about 0.01) is reported as unusable and the kernel evaluates erf instead.
 #include <math.h>
 #include <string.h>
 
@@ -82,18 +82,27 @@ static float first_true(float lo, float hi, P pred)
 static std::shared_ptr<GeluTable> build(float inv_so)
 {
     auto t = std::make_shared<GeluTable>();
-    // y below kLo: GELU(y) * inv_so rounds to 0; above hi: saturated at 127
-    const float kLo = -8.0f;
-    float hi = 130.0f / inv_so + 8.0f;
+    t->ok = false;
     t->nc = kGeluCells;
+    // The cells span only where the code can change: GELU falls from 0 to
+    // its minimum (near y = -0.75) and rises after it, so below some kLo <=
+    // -1 every code is 0 (the value only shrinks further left) and above some
+    // hi every code is 127. Both ends are found by bisection on the
+    // expression itself, with a margin; cells of (hi - kLo) / nc then stay
+    // narrower than the gap between code changes down to output scales of
+    // about 0.01.
+    const float far_hi = 130.0f / inv_so + 8.0f;
+    if (!isfinite(far_hi) || code_of(far_hi, inv_so) != 127 || code_of(-1e30f, inv_so) != 0) return t;
+    float kLo = -1.0f;
+    if (code_of(-1.0f, inv_so) != 0)
+        kLo = first_true(-1.0e30f, -1.0f, [&](float y) { return code_of(y, inv_so) != 0; }) - 0.5f;
+    const float hi = first_true(0.0f, far_hi, [&](float y) { return code_of(y, inv_so) == 127; }) + 0.5f;
     const float h = (hi - kLo) / (float)t->nc;
     t->hinv = 1.0f / h;
     // an integer offset keeps off exact next to kGeluBase
     t->off = kGeluBase + floorf(-kLo * t->hinv);
-    t->ok = false;
     if (!(isfinite(t->hinv) && isfinite(t->off))) return t;
-    if (code_of(kLo, inv_so) != 0 || code_of(-1e30f, inv_so) != 0) return t;
-    if (code_of(hi, inv_so) != 127) return t;
+    if (code_of(kLo, inv_so) != 0 || code_of(hi, inv_so) != 127) return t;
 
     float start = -3.0e38f;
     for (int c = 0; c < t->nc; ++c) {

@@ -1179,6 +1179,8 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int32_t x_la
         }
         if (st != SL_OK) return st;
     }
+    // the int8 GELU epilogue without a usable step table evaluates erf
+    if (run_kind == kEpiI8GeluErf) last_path() += " gelu=erf";
     return SL_OK;
 }
 

@@ -32,7 +32,10 @@ def _so_for(kind, x, w, sw, b):
     return float(oracle.calibrate_out_scale(g)) or 1.0
 
 
-@pytest.mark.parametrize("rows,cols", [(1, 1), (16, 32), (17, 33), (5, 100), (300, 768), (33, 3072), (4096, 768)])
+# 36 and 160 columns end in a partial block (padding features); 49152 x 768
+# makes the persistent grid loop over its pieces
+@pytest.mark.parametrize("rows,cols", [(1, 1), (16, 32), (17, 33), (5, 100), (3, 4), (31, 160), (48, 36),
+                                       (300, 768), (33, 3072), (4096, 768), (49152, 768)])
 def test_quantize_act_t16x32(hip, rows, cols):
     import torch
     rng = np.random.default_rng(rows + 7 * cols)

@@ -251,11 +251,13 @@ def test_workload_full_size_sampled(hip, name):
         del xd
 
 
-@pytest.mark.parametrize("so", [0.2, 0.05, 0.01, 3.0, 40.0])
+@pytest.mark.parametrize("so", [0.2, 0.05, 0.02, 0.015, 0.012, 0.01, 3.0, 40.0])
 def test_gelu_requant_across_output_scales(hip, so):
     """The int8 GELU epilogue over output scales that exercise the step table
-    (including codes of -1 in GELU's negative dip, so <= 0.34) and the erf
-    path the library falls back to when a table cell would hold two changes."""
+    (including codes of -1 in GELU's negative dip, so <= 0.34; the table
+    spans only where codes change, so it serves scales down to 0.015) and the
+    erf path the library falls back to below that, when a table cell would
+    hold two changes."""
     rng = np.random.default_rng(int(so * 1000))
     w = wk.random_block_sparse(256, 768, 0.15, rng)
     sw = rng.uniform(0.001, 0.01, 256).astype(np.float32)
@@ -264,7 +266,9 @@ def test_gelu_requant_across_output_scales(hip, so):
     pw = hip.PackedWeight.pack(w, sw, b)
     say(f"gelu requant so={so}")
     got = run_gpu(hip, pw, x, 0.02, 4, so)
+    path = hip.last_path()
     ref = oracle.linear(x, w, 0.02, sw, b, 4, so=so)
-    check(4, got, ref, f"i8_gelu so={so}")
+    check(4, got, ref, f"i8_gelu so={so} [{path}]")
+    assert path.endswith(" gelu=erf") == (so < 0.015), path
     if so <= 0.34:
         assert (ref == -1).any() or so > 0.3  # the dip reaches code -1
