@@ -127,3 +127,27 @@ def test_default_path_choice(hip, monkeypatch):
         rows = np.arange(0, m, max(1, m // 48))
         check(0, y.cpu().numpy()[rows], oracle.acc(np.ascontiguousarray(x[rows]), wd["w"]), f"{n}x{k} m={m}")
         pw.free()
+
+
+def test_panel_falls_back_when_no_panel_fits(hip, monkeypatch):
+    """A reduction too long for any channel group's panel to fit in LDS
+    (k = 16384: 128 windows, over 270 KB for two tiles) gets no panel image;
+    SL_PATH=panel then runs another kernel, with the same results."""
+    import torch
+    m, n, k = 20, 8, 16384
+    w, sw, b, rng = _case(n, k, 0.3, 11)
+    x = rng.integers(-127, 128, (m, k), dtype=np.int8)
+    pw = hip.PackedWeight.pack(w, sw, b)
+    monkeypatch.setenv("SL_PATH", "panel")
+    monkeypatch.delenv("SL_PTILE", raising=False)
+    for xl in (0, T):
+        xd = torch.from_numpy(np.ascontiguousarray(hip.to_t16x32(x, fill=5) if xl == T else x)).cuda()
+        for name in ("acc_i32", "f32"):
+            kind = KINDS[name]
+            say(f"no panel fits: k={k} layout={xl} {name}")
+            y = pw.run(xd, 0.02, kind, x_layout=xl, m_tokens=m)
+            torch.cuda.synchronize()
+            path = hip.last_path()
+            assert not path.startswith("panel"), path
+            check(kind, y.cpu().numpy(), oracle.linear(x, w, 0.02, sw, b, kind), f"{path} {name} layout={xl}")
+    pw.free()
