@@ -15,9 +15,9 @@
 // through the slice's token groups on their own: a wave loads its token rows
 // (the B operands) straight into registers, R - 1 windows ahead, reads the weight
 // operands from the resident panel, and multiplies an overflow operand only
-// where the window's mask says it exists. After the panel copy there is no
-// barrier, so one wave's epilogue overlaps the matrix instructions of the
-// others, and the weight image is read from memory once per workgroup rather
+// where the window's mask says it exists. Past the one barrier that follows
+// the panel copy and the set-up there is none, so one wave's epilogue
+// overlaps the matrix instructions of the others, and the weight image is read from memory once per workgroup rather
 // than once per token tile.
 #include <hip/hip_runtime.h>
 
