@@ -5,6 +5,10 @@ under ``profiles/``.
     python bench_profile.py stats --dir <rocprof dir> --bench-log <bench stdout> \
         --cmd "<the rocprofv3 command>" --out profiles/<kernel>_<workload>_kernel_trace.md
 
+    # per-launch averages of any counters (SQ waits, issue mix) from --pmc passes
+    python bench_profile.py counters --dir <dir> --log <stdout> --cmd "..." [--dir ... --log ... --cmd ...] \
+        --out profiles/<kernel>_<workload>_sq_counters.md
+
     # HBM bytes per launch from two counter runs of bench.py --copy-calib
     python bench_profile.py traffic --fetch <dir> --fetch-log <stdout> --write <dir> --write-log <stdout> \
         --cmd-fetch "..." --cmd-write "..." --out profiles/traffic.json --md profiles/<...>.md
@@ -191,6 +195,46 @@ def cmd_traffic(a):
         print("\n".join(lines))
 
 
+def cmd_counters(a):
+    """Average of each counter per launch of each op over the timed steps,
+    from one or more --pmc runs of bench.py (each pass its own directory and
+    stdout), with the wave-time shares of the SQ wait and issue counters."""
+    names = bench_names(a.workload)
+    avg = defaultdict(dict)
+    for d, log in zip(a.dir, a.log):
+        bl = _bench_line(log)
+        counters = sorted({r["Counter_Name"] for r in _rows(d, "counter_collection.csv")})
+        for c in counters:
+            vals, kn = _counter(d, c)
+            disp = [(k, kn[k], vals[k]) for k in vals if _is_lib_kernel(kn[k])]
+            timed, _, _ = _map_by_order(disp, names, bl)
+            for n in names:
+                v = timed.get(n, [])
+                if v:
+                    avg[n][c] = sum(v) / len(v)
+    lines = [f"# rocprofv3 counters: {a.title}", "", "Counter runs (from the repository root):", "", "```", *a.cmd,
+             "```", "", "Average per launch over the timed steps (SQ wave counters count units of 4 cycles, summed "
+             "over waves; SQ_VALU_MFMA_BUSY_CYCLES counts SIMD cycles):", ""]
+    counters = sorted({c for n in names for c in avg[n]})
+    lines += ["| counter | " + " | ".join(names) + " |", "|---|" + "---:|" * len(names)]
+    for c in counters:
+        lines.append(f"| {c} | " + " | ".join(f"{avg[n].get(c, float('nan')):.0f}" for n in names) + " |")
+    shares = [k for k in ("SQ_WAIT_ANY", "SQ_WAIT_INST_ANY", "SQ_ACTIVE_INST_ANY", "SQ_ACTIVE_INST_VALU",
+                          "SQ_ACTIVE_INST_SCA", "SQ_ACTIVE_INST_LDS", "SQ_ACTIVE_INST_VMEM")]
+    lines += ["", "Share of SQ_WAVE_CYCLES:", "", "| counter | " + " | ".join(names) + " |",
+              "|---|" + "---:|" * len(names)]
+    for c in shares:
+        row = []
+        for n in names:
+            wc = avg[n].get("SQ_WAVE_CYCLES")
+            row.append(f"{100.0 * avg[n][c] / wc:.1f} %" if wc and c in avg[n] else "-")
+        lines.append(f"| {c} | " + " | ".join(row) + " |")
+    lines += ["", f"Kernel source sha256[:16] = {bench.kernel_source_hash()}"]
+    with open(a.out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
     p = argparse.ArgumentParser()
     sub = p.add_subparsers(dest="what", required=True)
@@ -201,6 +245,13 @@ def main():
     s.add_argument("--out", required=True)
     s.add_argument("--title", default="")
     s.add_argument("--workload", default="c1")
+    c = sub.add_parser("counters")
+    c.add_argument("--dir", action="append", required=True, help="rocprof directory of one --pmc pass (repeat)")
+    c.add_argument("--log", action="append", required=True, help="stdout of that pass (holds the bench line)")
+    c.add_argument("--cmd", action="append", required=True, help="the rocprofv3 command of that pass")
+    c.add_argument("--out", required=True)
+    c.add_argument("--title", default="")
+    c.add_argument("--workload", default="c1")
     t = sub.add_parser("traffic")
     t.add_argument("--fetch", required=True)
     t.add_argument("--write", required=True)
@@ -213,7 +264,7 @@ def main():
     t.add_argument("--title", default="")
     t.add_argument("--workload", default="c1")
     a = p.parse_args()
-    {"stats": cmd_stats, "traffic": cmd_traffic}[a.what](a)
+    {"stats": cmd_stats, "traffic": cmd_traffic, "counters": cmd_counters}[a.what](a)
 
 
 if __name__ == "__main__":
