@@ -276,3 +276,48 @@ def test_hand_worked_example():
     assert np.array_equal(q, np.array(ex["q_i8"], np.int8))
     qg = oracle.linear(x, w, ex["sx"], sw, b, oracle.KIND_I8_GELU, so=ex["so"])
     assert np.array_equal(qg, np.array(ex["q_i8_gelu"], np.int8))
+
+
+def test_calibration_takes_the_magnitude_of_a_negative_extreme():
+    # Section "Post-training quantization": the per-tensor output scale maps the
+    # largest magnitude to code 127; a signed output whose extreme is negative
+    # must set it (g = [-3, 1, 2] -> max|g| = 3, so = 3/127 in fp32).
+    g = np.array([[-3.0, 1.0, 2.0]], np.float32)
+    assert oracle.absmax(g) == np.float32(3.0)
+    so = oracle.calibrate_out_scale(g)
+    assert so == np.float32(3.0) / np.float32(127.0)
+    # the extreme then maps to -127 exactly, the others by rounding
+    assert np.array_equal(oracle.quantize(g, so), np.array([[-127, 42, 85]], np.int8))
+    # a negative extreme far below every positive value
+    g2 = np.array([0.5, -100.0, 99.0, 0.0], np.float32)
+    assert oracle.absmax(g2) == np.float32(100.0)
+
+
+def test_chain_feeds_the_calibrated_output_scale_forward(monkeypatch):
+    """Hand-worked two-op chain: op b's input scale is op a's calibrated so.
+
+    Op a: x = [127, -64] with the seeded scale 0.02 and w_scale 50, so the
+    dequantisation scale fl(0.02 * 50) is exactly 1.0 and y = acc =
+    [127, -64, 63, 64]; so_a = 127 / 127 = 1.0 and the int8 codes equal y.
+    Op b reads those codes with x_scale = so_a = 1.0 and w_scale 0.5:
+    acc_b = [127, -64, 127, 63], y_b = acc_b * 0.5 + bias = [63.5, -32, 63.75, 31.5].
+    Had op b used the seeded scale 0.02 instead, y_b would be about 50x smaller.
+    """
+    from oracle import chain
+    import workloads as wk_mod
+
+    ops = (wk_mod.Op("a", 0, 4, 2, 0.0, "i8"), wk_mod.Op("b", 1, 4, 4, 0.0, "f32", "a"))
+    wl = wk_mod.Workload("hand", 9, 0, 1, 1, ops)
+    x_a = np.array([[127, -64]], np.int8)
+    monkeypatch.setattr(wk_mod, "op_seeded_x", lambda *a, **k: x_a.copy())
+    weights = {
+        "L0.a": {"w": np.array([[1, 0], [0, 1], [1, 1], [0, -1]], np.int8),
+                 "sw": np.full(4, 50.0, np.float32), "b": np.zeros(4, np.float32)},
+        "L0.b": {"w": np.array([[1, 0, 0, 0], [0, 1, 0, 0], [0, 0, 1, 1], [1, 0, 0, -1]], np.int8),
+                 "sw": np.full(4, 0.5, np.float32), "b": np.array([0, 0, 0.25, 0], np.float32)},
+    }
+    outs, scales, ins = chain.run(wl, weights=weights)
+    assert scales["L0.a"] == np.float32(1.0)
+    assert np.array_equal(outs["L0.a"], np.array([[127, -64, 63, 64]], np.int8))
+    assert ins["L0.b"][1] == np.float32(1.0)
+    assert np.array_equal(outs["L0.b"], np.array([[63.5, -32.0, 63.75, 31.5]], np.float32))
