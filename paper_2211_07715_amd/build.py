@@ -23,7 +23,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 HOST_SOURCES = ["api.cpp", "pack.cpp", "gelu_table.cpp"]
-HIP_SOURCES = ["kernels.hip", "kernels_direct.hip", "kernels_panel.hip"]
+HIP_SOURCES = ["kernels.hip", "kernels_direct.hip", "kernels_panel.hip", "kernels_resident.hip"]
 
 
 def _run(cmd, verbose):

@@ -157,10 +157,10 @@ struct EpiOut<SL_EPI_F32_GELU> {
 // biases of the 4 channels; tab, hinv, off, cmax (= kGeluBase + cells - 1):
 // the GELU step table.
 template <int KIND>
-__device__ __forceinline__ typename EpiOut<KIND>::T epilogue_value(const LinearArgs &a, const i32x4 acc,
-                                                                   const float s[4], const float b[4],
-                                                                   const GeluCell *tab, float hinv, float off,
-                                                                   float cmax)
+__device__ __forceinline__ typename EpiOut<KIND>::T epilogue_value_s(float inv_so, const i32x4 acc,
+                                                                     const float s[4], const float b[4],
+                                                                     const GeluCell *tab, float hinv, float off,
+                                                                     float cmax)
 {
 #pragma clang fp contract(off)
     if constexpr (KIND == SL_EPI_ACC_I32) {
@@ -193,10 +193,19 @@ __device__ __forceinline__ typename EpiOut<KIND>::T epilogue_value(const LinearA
         } else {
             uint32_t packed = 0;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) packed |= ((uint32_t)requant_i8(g[r], a.inv_so) & 0xffu) << (8 * r);
+            for (int r = 0; r < 4; ++r) packed |= ((uint32_t)requant_i8(g[r], inv_so) & 0xffu) << (8 * r);
             return packed;
         }
     }
+}
+
+template <int KIND>
+__device__ __forceinline__ typename EpiOut<KIND>::T epilogue_value(const LinearArgs &a, const i32x4 acc,
+                                                                   const float s[4], const float b[4],
+                                                                   const GeluCell *tab, float hinv, float off,
+                                                                   float cmax)
+{
+    return epilogue_value_s<KIND>(a.inv_so, acc, s, b, tab, hinv, off, cmax);
 }
 
 // Epilogue and store of one accumulator group at token tok, channels
@@ -320,5 +329,60 @@ sl_status panel_resident(PanelCfg c, size_t lds, int *out);
 // use per device it also raises the kernel's dynamic-LDS limit; cache holds
 // kMaxDevices entries per kernel instance.
 sl_status persistent_grid(const void *fn, int threads, size_t lds, int *cache, int *out);
+
+// ---------------------------------------------------------------------------
+// Register-resident kernel (kernels_resident.hip): 4 waves, one per SIMD;
+// wave w owns channel part w / ks (kResTiles tiles) and K slice w % ks
+// (kResWin windows) of its workgroup's channel group, whose main operands it
+// holds in registers; token passes of 16 ST tokens stream through LDS.
+constexpr int kResWaves = 4;
+constexpr int kResThreads = 64 * kResWaves;
+
+struct ResArgs {
+    const int8_t *x;
+    void *y;
+    int64_t m;             // tokens of this launch
+    int32_t n, k;
+    const int8_t *main;    // main operands [n_win][n_tiles][kOpBytes]
+    uint32_t main_bytes;
+    const int8_t *rovf;    // consolidated overflow operands [res_ops][kResOpBytes]
+    uint32_t rovf_bytes;
+    const uint32_t *rdir;  // [n_tiles * ks + 1]
+    const float *w_scale;
+    const float *bias;
+    float sx;
+    float inv_so;
+    int32_t n_tiles, n_win;
+    int32_t ks;            // waves a reduction is split over: 1, 2 or 4
+    int32_t tiles_wg;      // channel tiles per workgroup: (kResWaves / ks) * kResTiles
+    int32_t n_cg;          // channel groups
+    int32_t wg_per_cg;     // workgroups (token slices) per channel group
+    int32_t passes;        // token passes of this launch (16 ST tokens each)
+    int32_t x_cb;          // 32-feature column blocks of x (block layout)
+    int32_t y_cb;          // 32-channel column blocks of y (block layout)
+    int32_t cbw;           // 32-column blocks of the LDS token tile: 4 n_win
+    int32_t xt, yt;        // x / y in SL_LAYOUT_T16X32
+    uint32_t lds_ovf;      // LDS bytes for the overflow operands (a multiple of 1024)
+};
+
+// LDS layout of a launch (byte offsets, all multiples of 16): two token-tile
+// buffers, the group's scales and biases, the GELU table, the partial sums of
+// a split reduction, the consolidated overflow operands
+struct ResLds {
+    uint32_t xbuf, vec, tab, red, ovf, total;
+};
+__host__ __device__ inline ResLds res_lds_layout(int st, int cbw, int tiles_wg, int ks, bool gelu, uint32_t ovf_bytes)
+{
+    ResLds l;
+    l.xbuf = (uint32_t)st * (uint32_t)cbw * 512u;
+    l.vec = 2 * l.xbuf;
+    l.tab = l.vec + (uint32_t)tiles_wg * kTileN * 8u;
+    l.red = l.tab + (gelu ? (uint32_t)kGeluLds : 0u);
+    l.ovf = l.red + (ks > 1 ? (uint32_t)kResWaves * kResTiles * (uint32_t)st * 1024u : 0u);
+    l.total = l.ovf + ovf_bytes;
+    return l;
+}
+sl_status launch_resident(const ResArgs &a, const GeluArg *ep, int32_t run_kind, int st, uint32_t grid, size_t lds,
+                          hipStream_t stream);
 
 }  // namespace sl
