@@ -1098,8 +1098,7 @@ static sl_status try_resident(const sl_packed_weight *w, const LinearArgs &la, b
     a.ks = ti.res_ks;
     a.tiles_wg = (kResWaves / a.ks) * kResTiles;
     a.n_cg = (a.n_tiles + a.tiles_wg - 1) / a.tiles_wg;
-    const int st = 1;
-    a.passes = (int32_t)std::min<int64_t>((a.m + 16 * st - 1) / (16 * st), INT32_MAX);
+    a.passes = (int32_t)std::min<int64_t>((a.m + 15) / 16, INT32_MAX);
     int dev = 0, n_cu = 0;
     HIP_TRY(hipGetDevice(&dev));
     HIP_TRY(hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev));
@@ -1110,15 +1109,15 @@ static sl_status try_resident(const sl_packed_weight *w, const LinearArgs &la, b
     a.xt = xt ? 1 : 0;
     a.yt = yt ? 1 : 0;
     a.lds_ovf = w->dev.res_lds_ovf;
-    const ResLds L = res_lds_layout(st, a.cbw, a.tiles_wg, a.ks, run_kind == SL_EPI_I8_GELU, a.lds_ovf);
+    const int out_bytes = (run_kind == SL_EPI_I8 || run_kind == SL_EPI_I8_GELU || run_kind == kEpiI8GeluErf) ? 1 : 4;
+    const ResLds L = res_lds_layout(a.cbw, a.tiles_wg, a.ks, out_bytes, run_kind == SL_EPI_I8_GELU, a.lds_ovf);
     if (L.total > kLdsMax) return SL_ERR_UNSUPPORTED;
     const int64_t grid = (int64_t)a.n_cg * a.wg_per_cg;
     if (grid > 0x7fffffff) return SL_ERR_UNSUPPORTED;
-    sl_status st_ = launch_resident(a, ep, run_kind, st, (uint32_t)grid, L.total, s);
+    sl_status st_ = launch_resident(a, ep, run_kind, (uint32_t)grid, L.total, s);
     if (st_ != SL_OK) return st_;
-    last_path() = "resident ks=" + std::to_string(a.ks) + " st=" + std::to_string(st) +
-                  " groups=" + std::to_string(a.n_cg) + "x" + std::to_string(a.wg_per_cg) + " lds=" +
-                  std::to_string(L.total);
+    last_path() = "resident ks=" + std::to_string(a.ks) + " groups=" + std::to_string(a.n_cg) + "x" +
+                  std::to_string(a.wg_per_cg) + " lds=" + std::to_string(L.total);
     return SL_OK;
 }
 

@@ -331,12 +331,13 @@ sl_status panel_resident(PanelCfg c, size_t lds, int *out);
 sl_status persistent_grid(const void *fn, int threads, size_t lds, int *cache, int *out);
 
 // ---------------------------------------------------------------------------
-// Register-resident kernel (kernels_resident.hip): 4 waves, one per SIMD;
-// wave w owns channel part w / ks (kResTiles tiles) and K slice w % ks
-// (kResWin windows) of its workgroup's channel group, whose main operands it
-// holds in registers; token passes of 16 ST tokens stream through LDS.
-constexpr int kResWaves = 4;
-constexpr int kResThreads = 64 * kResWaves;
+// Register-resident kernel (kernels_resident.hip): 4 compute waves, one per
+// SIMD, and one memory wave; compute wave w owns channel part w / ks
+// (kResTiles tiles) and K slice w % ks (kResWin windows) of its workgroup's
+// channel group, whose main operands it holds in registers; token passes of
+// 16 tokens stream through LDS.
+constexpr int kResWaves = 4;                   // compute waves
+constexpr int kResThreads = 64 * (kResWaves + 1);
 
 struct ResArgs {
     const int8_t *x;
@@ -353,11 +354,11 @@ struct ResArgs {
     float sx;
     float inv_so;
     int32_t n_tiles, n_win;
-    int32_t ks;            // waves a reduction is split over: 1, 2 or 4
+    int32_t ks;            // compute waves a reduction is split over: 1, 2 or 4
     int32_t tiles_wg;      // channel tiles per workgroup: (kResWaves / ks) * kResTiles
     int32_t n_cg;          // channel groups
     int32_t wg_per_cg;     // workgroups (token slices) per channel group
-    int32_t passes;        // token passes of this launch (16 ST tokens each)
+    int32_t passes;        // token passes of this launch (16 tokens each)
     int32_t x_cb;          // 32-feature column blocks of x (block layout)
     int32_t y_cb;          // 32-channel column blocks of y (block layout)
     int32_t cbw;           // 32-column blocks of the LDS token tile: 4 n_win
@@ -366,23 +367,40 @@ struct ResArgs {
 };
 
 // LDS layout of a launch (byte offsets, all multiples of 16): two token-tile
-// buffers, the group's scales and biases, the GELU table, the partial sums of
-// a split reduction, the consolidated overflow operands
+// buffers (16 tokens x all columns each); two output staging buffers (16 token
+// rows of the group's channels, out_bytes each, rows ostride bytes apart); the
+// group's scales and biases; the GELU table; the index words of the group's
+// main operands ([tile][window][16 words]); an all-zero overflow operand
+// (stands in for an absent one); the partial sums of a split reduction (in
+// the pass's own token-tile buffer when it is large enough: every wave has
+// finished reading it by then); the consolidated overflow operands.
 struct ResLds {
-    uint32_t xbuf, vec, tab, red, ovf, total;
+    uint32_t xbuf, out, ostride, obuf, vec, tab, idx, dummy, red, ovf, total;
 };
-__host__ __device__ inline ResLds res_lds_layout(int st, int cbw, int tiles_wg, int ks, bool gelu, uint32_t ovf_bytes)
+constexpr uint32_t kResRedBytes = (uint32_t)kResWaves * kResTiles * 1024u;
+__host__ __device__ inline ResLds res_lds_layout(int cbw, int tiles_wg, int ks, int out_bytes, bool gelu,
+                                                 uint32_t ovf_bytes)
 {
     ResLds l;
-    l.xbuf = (uint32_t)st * (uint32_t)cbw * 512u;
-    l.vec = 2 * l.xbuf;
+    l.xbuf = (uint32_t)cbw * 512u;
+    l.out = 2 * l.xbuf;
+    l.ostride = (uint32_t)tiles_wg * kTileN * (uint32_t)out_bytes + 16u;
+    l.obuf = 16u * l.ostride;
+    l.vec = l.out + 2 * l.obuf;
     l.tab = l.vec + (uint32_t)tiles_wg * kTileN * 8u;
-    l.red = l.tab + (gelu ? (uint32_t)kGeluLds : 0u);
-    l.ovf = l.red + (ks > 1 ? (uint32_t)kResWaves * kResTiles * (uint32_t)st * 1024u : 0u);
+    l.idx = l.tab + (gelu ? (uint32_t)kGeluLds : 0u);
+    l.dummy = l.idx + (uint32_t)tiles_wg * (uint32_t)(cbw / 4) * 64u;
+    uint32_t end = l.dummy + (uint32_t)kResOpBytes;
+    l.red = 0xffffffffu;  // in the pass's token-tile buffer
+    if (ks > 1 && l.xbuf < kResRedBytes) {
+        l.red = end;
+        end += kResRedBytes;
+    }
+    l.ovf = end;
     l.total = l.ovf + ovf_bytes;
     return l;
 }
-sl_status launch_resident(const ResArgs &a, const GeluArg *ep, int32_t run_kind, int st, uint32_t grid, size_t lds,
+sl_status launch_resident(const ResArgs &a, const GeluArg *ep, int32_t run_kind, uint32_t grid, size_t lds,
                           hipStream_t stream);
 
 }  // namespace sl

@@ -69,7 +69,7 @@ struct TileImage {
     std::vector<uint32_t> res_dir;
 };
 
-constexpr int kResTiles = 6;  // channel tiles per wave
+constexpr int kResTiles = 5;  // channel tiles per wave
 constexpr int kResWin = 6;    // 128-column windows per wave
 constexpr int kResOpBytes = kOpBytes + 128;  // 1216 = 76 pieces of 16 bytes
 constexpr int kResMaxKs = 4;
