@@ -37,7 +37,7 @@
 extern "C" {
 #endif
 
-#define SL_ABI_VERSION 2
+#define SL_ABI_VERSION 3
 
 typedef enum {
     SL_OK = 0,
@@ -137,6 +137,12 @@ sl_status sparse_linear_pack_host(const int8_t *w_host, int32_t n_out, int32_t k
  *                 (else SL_ERR_INVALID_ARG).
  *   hip_stream    a hipStream_t (NULL = the legacy default stream).
  * The caller keeps X and Y alive until the stream has passed the call.
+ * Host cost: the first SL_EPI_I8_GELU run at a given out_scale builds that
+ * scale's GELU step table on the host (under 1 ms of one core, typically;
+ * up to about 50 ms where it checks every fp32 value of a cell; under a
+ * lock that serialises concurrent first uses); the library keeps the 32 most
+ * recently built tables in static storage and rebuilds one that has been
+ * displaced. No other run allocates or builds anything on the host.
  */
 sl_status sparse_linear_run(const sl_packed_weight *w, const int8_t *x_dev, int64_t m_tokens,
                             float x_scale, int32_t epilogue_kind, float out_scale, void *y_dev,
@@ -228,6 +234,27 @@ int32_t sl_abi_version(void);
  * the next run on this thread.
  */
 const char *sl_last_path(void);
+
+/*
+ * Kernel selection overrides, for tuning and tests: SL_PATH (panel, direct,
+ * staged, resident) and the tile shapes SL_TILE / SL_DTILE / SL_PTILE are
+ * read from the environment once, at the first run; sl_reload_env() reads
+ * them again (call it after changing them, with no run in flight on any
+ * thread).
+ */
+void sl_reload_env(void);
+
+/*
+ * Host evaluation of the step table that SL_EPI_I8_GELU runs use in place of
+ * erf (Appendix "Graph optimization": GELU fused into the InnerProduct,
+ * followed by requantisation as in Section "Sparse GEMM operators"):
+ * q[i] = the table's code for the dequantised value y[i] at this out_scale,
+ * looked up exactly as the kernels look it up. Host pointers, n >= 0.
+ * Returns SL_ERR_UNSUPPORTED when out_scale admits no table (the kernels
+ * then evaluate erf), SL_ERR_INVALID_ARG for a bad scale or NULL pointers.
+ * For tests of the table against the definition.
+ */
+sl_status sl_gelu_table_codes(float out_scale, const float *y, int8_t *q, int64_t n);
 
 #ifdef __cplusplus
 }

@@ -42,7 +42,11 @@ EXPORTS = ("sparse_linear_pack", "sparse_linear_pack_host", "sparse_linear_run",
            "quantize_act", "quantize_act_layout",
            "sparse_linear_unpack", "sparse_linear_info", "sparse_linear_export_bsr",
            "sparse_linear_tile_stats", "sparse_linear_free", "sl_status_string", "sl_last_error",
-           "sl_abi_version", "sl_last_path")
+           "sl_abi_version", "sl_last_path", "sl_reload_env", "sl_gelu_table_codes")
+
+# kernel-selection overrides the library reads from the environment
+ENV_KEYS = ("SL_PATH", "SL_TILE", "SL_DTILE", "SL_PTILE")
+_env_seen: Optional[tuple] = None
 
 _lib: Optional[ctypes.CDLL] = None
 
@@ -88,8 +92,22 @@ def load() -> ctypes.CDLL:
     lib.sl_abi_version.restype = i32
     lib.sl_last_path.argtypes = []
     lib.sl_last_path.restype = ctypes.c_char_p
+    lib.sl_reload_env.argtypes = []
+    lib.sl_reload_env.restype = None
+    lib.sl_gelu_table_codes.argtypes = [f32, vp, vp, i64]
+    lib.sl_gelu_table_codes.restype = i32
     _lib = lib
     return lib
+
+
+def _sync_env(lib: ctypes.CDLL):
+    """The library reads SL_PATH / SL_*TILE once; have it read them again when
+    this process has changed them since the last run."""
+    global _env_seen
+    now = tuple(os.environ.get(k) for k in ENV_KEYS)
+    if now != _env_seen:
+        lib.sl_reload_env()
+        _env_seen = now
 
 
 def _check(status: int, where: str):
@@ -232,7 +250,9 @@ class PackedWeight:
             out = torch.empty(shape, dtype=dt, device=x.device)
         elif out.dtype != dt or tuple(out.shape) != tuple(shape) or not out.is_contiguous():
             raise ValueError("out has the wrong dtype/shape or is not contiguous")
-        _check(load().sparse_linear_run_layout(self.handle, ctypes.c_void_p(x.data_ptr()), int(x_layout), m,
+        lib = load()
+        _sync_env(lib)
+        _check(lib.sparse_linear_run_layout(self.handle, ctypes.c_void_p(x.data_ptr()), int(x_layout), m,
                                                float(x_scale), int(kind), float(out_scale),
                                                ctypes.c_void_p(out.data_ptr()), int(y_layout), _stream_ptr(stream)),
                "sparse_linear_run_layout")
@@ -242,6 +262,19 @@ class PackedWeight:
 def last_path() -> str:
     """Kernel and workgroup shape of the last successful run on this thread."""
     return load().sl_last_path().decode()
+
+
+def gelu_table_codes(out_scale: float, y: np.ndarray) -> Optional[np.ndarray]:
+    """int8 codes of the GELU + requantisation step table for fp32 values y,
+    looked up as the kernels do; None when out_scale admits no table."""
+    lib = load()
+    y = np.ascontiguousarray(y, dtype=np.float32)
+    q = np.empty(y.shape, dtype=np.int8)
+    st = lib.sl_gelu_table_codes(float(out_scale), _np_ptr(y), _np_ptr(q), y.size)
+    if st == -5:
+        return None
+    _check(st, "sl_gelu_table_codes")
+    return q
 
 
 def quantize_act(x, scale: float, out=None, stream=None, layout: int = LAYOUT_ROWS):

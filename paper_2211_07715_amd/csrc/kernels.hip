@@ -616,8 +616,7 @@ sl_status check_device_arch(int *device)
     hipDeviceProp_t prop;
     HIP_TRY(hipGetDeviceProperties(&prop, dev));
     if (strncmp(prop.gcnArchName, "gfx950", 6) != 0) {
-        set_error(std::string("device ") + std::to_string(dev) + " is " + prop.gcnArchName +
-                  "; this library has gfx950 kernels only");
+        set_error("device %d is %s; this library has gfx950 kernels only", dev, prop.gcnArchName);
         return SL_ERR_UNSUPPORTED;
     }
     *device = dev;
@@ -782,7 +781,7 @@ sl_status upload_image(sl_packed_weight *w)
     void *base = nullptr;
     hipError_t e = hipMalloc(&base, total);
     if (e != hipSuccess) {
-        set_error(std::string("hipMalloc of the packed weight: ") + hipGetErrorString(e));
+        set_error("hipMalloc of the packed weight: %s", hipGetErrorString(e));
         return e == hipErrorOutOfMemory ? SL_ERR_OOM : SL_ERR_HIP;
     }
     char *p = static_cast<char *>(base);
@@ -923,13 +922,10 @@ static sl_status launch_vec(const LinearArgs &a, const GeluArg *ep, TileCfg c, h
 // overrides (tuning; unknown shapes are ignored).
 static TileCfg choose_cfg(int64_t m, const sl_packed_weight *w)
 {
-    const char *env = getenv("SL_TILE");
-    if (env) {
-        TileCfg c;
-        if (sscanf(env, "%d,%d,%d,%d,%d", &c.st, &c.ct, &c.wm, &c.wn, &c.d) == 5)
-            for (const TileCfg &k : kCfgs)
-                if (k.st == c.st && k.ct == c.ct && k.wm == c.wm && k.wn == c.wn && k.d == c.d) return k;
-    }
+    const int *e = env_cfg().tile;
+    if (e[0])
+        for (const TileCfg &k : kCfgs)
+            if (k.st == e[0] && k.ct == e[1] && k.wm == e[2] && k.wn == e[3] && k.d == e[4]) return k;
     const int32_t n_tiles = w->tiles.n_tiles;
     const double xbytes = (double)m * w->k_in;
     const double wbytes = (double)w->tiles.main.size() + (double)w->tiles.ovf.size();
@@ -958,13 +954,10 @@ static TileCfg choose_cfg(int64_t m, const sl_packed_weight *w)
 // Direct-kernel shape, by the same rule; SL_DTILE="st,nt,wm,d" overrides.
 static DirectCfg choose_direct_cfg(int64_t m, const sl_packed_weight *w)
 {
-    const char *env = getenv("SL_DTILE");
-    if (env) {
-        DirectCfg c;
-        if (sscanf(env, "%d,%d,%d,%d", &c.st, &c.nt, &c.wm, &c.d) == 4)
-            for (const DirectCfg &k : kDirectCfgs)
-                if (k.st == c.st && k.nt == c.nt && k.wm == c.wm && k.d == c.d) return k;
-    }
+    const int *e = env_cfg().dtile;
+    if (e[0])
+        for (const DirectCfg &k : kDirectCfgs)
+            if (k.st == e[0] && k.nt == e[1] && k.wm == e[2] && k.d == e[3]) return k;
     const int32_t n_tiles = w->tiles.n_tiles;
     const double xbytes = (double)m * w->k_in;
     const double wbytes = (double)w->tiles.main.size() + (double)w->tiles.ovf.size();
@@ -1004,10 +997,9 @@ static sl_status choose_panel_cfg(LinearArgs &a, const sl_packed_weight *w, int3
     int n_cu = 0, dev = 0;
     HIP_TRY(hipGetDevice(&dev));
     HIP_TRY(hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev));
-    const char *env = getenv("SL_PTILE");
-    PanelCfg forced{};
-    const bool have_forced =
-        env && sscanf(env, "%d,%d,%d,%d", &forced.nt, &forced.st, &forced.nwv, &forced.r) == 4;
+    const int *e = env_cfg().ptile;
+    const PanelCfg forced{e[0], e[1], e[2], e[3]};
+    const bool have_forced = e[0] != 0;
     const int64_t mpad = (a.m + 15) / 16 * 16;
     double best_cost = 0;
     bool found = false;
@@ -1116,8 +1108,7 @@ static sl_status try_resident(const sl_packed_weight *w, const LinearArgs &la, b
     if (grid > 0x7fffffff) return SL_ERR_UNSUPPORTED;
     sl_status st_ = launch_resident(a, ep, run_kind, (uint32_t)grid, L.total, s);
     if (st_ != SL_OK) return st_;
-    last_path() = "resident ks=" + std::to_string(a.ks) + " groups=" + std::to_string(a.n_cg) + "x" +
-                  std::to_string(a.wg_per_cg) + " lds=" + std::to_string(L.total);
+    set_last_path("resident ks=%d groups=%dx%d lds=%u", a.ks, a.n_cg, a.wg_per_cg, L.total);
     return SL_OK;
 }
 
@@ -1127,8 +1118,7 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int32_t x_la
     int dev = -1;
     HIP_TRY(hipGetDevice(&dev));
     if (dev != w->dev.device) {
-        set_error("handle was packed on device " + std::to_string(w->dev.device) + ", current device is " +
-                  std::to_string(dev));
+        set_error("handle was packed on device %d, current device is %d", w->dev.device, dev);
         return SL_ERR_INVALID_ARG;
     }
     const TileImage &ti = w->tiles;
@@ -1153,16 +1143,17 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int32_t x_la
     a.slice_groups = 0;
     hipStream_t s = static_cast<hipStream_t>(stream);
 
+    // (host stack only: the step table is copied out of a fixed-size cache)
     GeluArg ga;
     int32_t run_kind = kind;
     if (kind == SL_EPI_I8_GELU) {
-        std::shared_ptr<const GeluTable> tab = gelu_table(inv_so);
-        if (tab->ok) {
-            ga.hinv = tab->hinv;
-            ga.off = tab->off;
-            ga.nc = tab->nc;
+        GeluTable tab;
+        if (gelu_table(inv_so, &tab)) {
+            ga.hinv = tab.hinv;
+            ga.off = tab.off;
+            ga.nc = tab.nc;
             ga.pad = 0;
-            memcpy(ga.cell, tab->cell, sizeof(ga.cell));
+            memcpy(ga.cell, tab.cell, sizeof(ga.cell));
         } else {
             run_kind = kEpiI8GeluErf;
         }
@@ -1189,14 +1180,14 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int32_t x_la
         // block-layout output from aligned rows) or the staged kernel
         // (row-major input and output). SL_PATH=panel|direct|staged forces a
         // kernel (tests, tuning; panel falls back when no panel fits).
-        const char *path = getenv("SL_PATH");
-        if (vec && path && strcmp(path, "resident") == 0) {
+        const char *path = env_cfg().path;
+        if (vec && strcmp(path, "resident") == 0) {
             sl_status rst = try_resident(w, a, xt, yt, run_kind, run_kind == SL_EPI_I8_GELU ? &ga : nullptr, s);
             if (rst == SL_OK) continue;
             if (rst != SL_ERR_UNSUPPORTED) return rst;
         }
-        const bool force_panel = path && strcmp(path, "panel") == 0;
-        const bool auto_path = !path || !*path;
+        const bool force_panel = strcmp(path, "panel") == 0;
+        const bool auto_path = !*path;
         if (vec && (force_panel || (auto_path && ti.n_win <= kPanelMaxWin))) {
             PanelCfg pc{};
             size_t lds = 0;
@@ -1206,17 +1197,14 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int32_t x_la
             if (pst == SL_OK) {
                 pst = launch_panel(a, run_kind == SL_EPI_I8_GELU ? &ga : nullptr, run_kind, pc, xt, yt, lds, s);
                 if (pst != SL_OK) return pst;
-                last_path() = "panel " + std::to_string(pc.nt) + "," + std::to_string(pc.st) + "," +
-                              std::to_string(pc.nwv) + "," + std::to_string(pc.r) +
-                              " groups=" + std::to_string(a.n_cgroups) +
-                              " slices=" + std::to_string(a.n_slices) + "x" + std::to_string(a.slice_groups) +
-                              " lds=" + std::to_string(lds);
+                set_last_path("panel %d,%d,%d,%d groups=%d slices=%dx%d lds=%zu", pc.nt, pc.st, pc.nwv, pc.r,
+                              a.n_cgroups, a.n_slices, a.slice_groups, lds);
                 continue;
             }
             if (pst != SL_ERR_UNSUPPORTED) return pst;
         }
-        const bool direct = (xt || (yt && vec) || (vec && path && strcmp(path, "direct") == 0)) &&
-                            !(path && strcmp(path, "staged") == 0 && !xt && !yt);
+        const bool direct = (xt || (yt && vec) || (vec && strcmp(path, "direct") == 0)) &&
+                            !(strcmp(path, "staged") == 0 && !xt && !yt);
         TileCfg cfg{};
         DirectCfg dcfg{};
         int nt, tm;
@@ -1246,11 +1234,9 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int32_t x_la
         sl_status st;
         if (direct) {
             st = launch_direct(a, run_kind == SL_EPI_I8_GELU ? &ga : nullptr, run_kind, dcfg, xt, yt, s);
-            last_path() = "direct " + std::to_string(dcfg.st) + "," + std::to_string(dcfg.nt) + "," +
-                          std::to_string(dcfg.wm) + "," + std::to_string(dcfg.d);
+            set_last_path("direct %d,%d,%d,%d", dcfg.st, dcfg.nt, dcfg.wm, dcfg.d);
         } else {
-            last_path() = "staged " + std::to_string(cfg.st) + "," + std::to_string(cfg.ct) + "," +
-                          std::to_string(cfg.wm) + "," + std::to_string(cfg.wn) + "," + std::to_string(cfg.d);
+            set_last_path("staged %d,%d,%d,%d,%d", cfg.st, cfg.ct, cfg.wm, cfg.wn, cfg.d);
             switch (run_kind) {
             case SL_EPI_ACC_I32: st = launch_vec<SL_EPI_ACC_I32>(a, nullptr, cfg, s, vec, yt); break;
             case SL_EPI_F32: st = launch_vec<SL_EPI_F32>(a, nullptr, cfg, s, vec, yt); break;
@@ -1263,7 +1249,7 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int32_t x_la
         if (st != SL_OK) return st;
     }
     // the int8 GELU epilogue without a usable step table evaluates erf
-    if (run_kind == kEpiI8GeluErf) last_path() += " gelu=erf";
+    if (run_kind == kEpiI8GeluErf) append_last_path(" gelu=erf");
     return SL_OK;
 }
 

@@ -46,11 +46,11 @@ sl_status validate_weight_args(const int8_t *w, int32_t n_out, int32_t k_in, int
     }
     for (int32_t n = 0; n < n_out; ++n) {
         if (!(isfinite(w_scale[n]) && w_scale[n] > 0.0f)) {
-            set_error("w_scale must be finite and > 0 (channel " + std::to_string(n) + ")");
+            set_error("w_scale must be finite and > 0 (channel %d)", (int)n);
             return SL_ERR_INVALID_ARG;
         }
         if (bias && !isfinite(bias[n])) {
-            set_error("bias must be finite (channel " + std::to_string(n) + ")");
+            set_error("bias must be finite (channel %d)", (int)n);
             return SL_ERR_INVALID_ARG;
         }
     }

@@ -47,7 +47,7 @@ constexpr size_t kLdsMax = 160 * 1024; // LDS per workgroup on gfx950
     do {                                                                                  \
         hipError_t e_ = (expr);                                                           \
         if (e_ != hipSuccess) {                                                           \
-            set_error(std::string(#expr) + ": " + hipGetErrorString(e_));                 \
+            set_error("%s: %s", #expr, hipGetErrorString(e_));                              \
             return SL_ERR_HIP;                                                            \
         }                                                                                 \
     } while (0)

@@ -100,7 +100,12 @@ struct GeluTable {
     bool ok = false;          // false: a cell would hold two changes; use erf
     GeluCell cell[kGeluCells];
 };
-std::shared_ptr<const GeluTable> gelu_table(float inv_so);
+// The step table for inverse output scale inv_so from a fixed-size cache
+// (built on first use of inv_so, under a lock; no allocation), copied into
+// *out. Returns out->ok.
+bool gelu_table(float inv_so, GeluTable *out);
+// the code the table gives for y (host copy of the kernels' lookup)
+int gelu_table_code(const GeluTable &t, float y);
 
 // Per tile-group size nt (channel tiles per workgroup): for every window w and
 // group g, the pair (mask, first): bit j of mask set if tile g*nt + j has an
@@ -166,12 +171,26 @@ struct sl_packed_weight {
 
 namespace sl {
 
-// thread-local name of the last launched kernel shape (sl_last_path)
-std::string &last_path();
+// thread-local name of the last launched kernel shape (sl_last_path), written
+// printf-style into a fixed buffer: no allocation on the run path
+void set_last_path(const char *fmt, ...) __attribute__((format(printf, 1, 2)));
+void append_last_path(const char *text);
+const char *last_path();
 
-// thread-local error text
-void set_error(const std::string &msg);
+// thread-local error text, printf-style into a fixed buffer
+void set_error(const char *fmt, ...) __attribute__((format(printf, 1, 2)));
 void clear_error();
+
+// Kernel-choice overrides for tests and tuning (SL_PATH, SL_TILE, SL_DTILE,
+// SL_PTILE), read from the environment once and again on sl_reload_env()
+struct EnvCfg {
+    char path[16];  // "" (automatic), "panel", "direct", "staged", "resident"
+    int tile[5];    // SL_TILE "st,ct,wm,wn,d"; tile[0] == 0: unset
+    int dtile[4];   // SL_DTILE "st,nt,wm,d"
+    int ptile[4];   // SL_PTILE "nt,st,nwv,r"
+};
+const EnvCfg &env_cfg();
+void reload_env();
 
 // host packer (pack.cpp)
 sl_status validate_weight_args(const int8_t *w, int32_t n_out, int32_t k_in, int32_t bh, int32_t bw,

@@ -31,7 +31,7 @@ def test_library_exports_every_declared_symbol():
     assert declared == set(sl.EXPORTS), declared ^ set(sl.EXPORTS)
     for name in declared:
         assert hasattr(lib, name), name
-    assert lib.sl_abi_version() == 2
+    assert lib.sl_abi_version() == 3
     assert lib.sl_status_string(-2) == b"SL_ERR_SHAPE"
 
 
