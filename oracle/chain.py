@@ -12,7 +12,7 @@ gives exact oracle values for sampled outputs of very large batches.
 """
 from __future__ import annotations
 
-from typing import Dict, Optional, Sequence
+from typing import Dict, Iterator, Optional, Sequence
 
 import numpy as np
 
@@ -27,6 +27,34 @@ _KIND = {"f32": oracle.KIND_F32, "f32_gelu": oracle.KIND_F32_GELU,
 
 def op_key(layer: int, name: str) -> str:
     return f"L{layer}.{name}"
+
+
+def steps(wl: wk.Workload, calib: Dict[str, float], seed: int = 0) -> Iterator[tuple]:
+    """The chain one op at a time with stored output scales, holding only the
+    outputs a later op still reads (for very large batches). Yields
+    (key, x, sx, kind, so, acc, y): the op's int8 input and its scale, the
+    oracle kind, the output scale (1.0 for fp32 kinds), the int32
+    accumulators and the final output. The layer is the contraction followed
+    by the epilogue (Section "Sparse GEMM operators"), so y is computed from
+    acc by the oracle's epilogue: the same values oracle.linear gives."""
+    later = {wl.op_src(l2, o2) for l2, o2 in wk.op_list(wl)} - {"seeded"}
+    outs: Dict[str, np.ndarray] = {}
+    for layer, op in wk.op_list(wl):
+        key = op_key(layer, op.name)
+        src = wl.op_src(layer, op)
+        if src == "seeded":
+            x, sx = wk.op_seeded_x(wl, layer, op, seed=seed), float(wk.SX)
+        else:
+            x, sx = outs[src], float(calib[src])
+        wd = wk.op_weight(wl, layer, op, seed=seed)
+        kname = wl.op_kind(layer, op)
+        so = float(calib[key]) if kname in ("i8", "i8_gelu") else 1.0
+        acc = oracle.acc(x, wd["w"])
+        y = oracle.epilogue(acc, sx, wd["sw"], wd["b"], _KIND[kname], so=so)
+        if key in later:
+            outs[key] = y
+        yield key, wd, x, sx, _KIND[kname], so, acc, y
+        del acc
 
 
 def run(wl: wk.Workload, calib: Optional[Dict[str, float]] = None, rows: Optional[Sequence[int]] = None,

@@ -164,3 +164,75 @@ def test_chain_in_block_layout(hip, name):
             got = hip.from_t16x32(got, wl.m, op.n_out)
         check(kind, got, outs[key], f"{name} {key}")
         pw.free()
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name", ["c4", "c4_bertl"])
+def test_full_size_chain_in_block_layout(hip, name):
+    """M = 49152 tokens, every row of every op: each op reads the oracle's own
+    input for it (the chained int8 output of the op before, or its seeded
+    input) in the block layout, int8 outputs are written in it, and the int32
+    accumulators of every op are compared too, bit for bit."""
+    import torch
+    wl = wk.workloads()[name]
+    calib = _calib()[name]
+    for key, wd, x, sx, kind, so, acc, ref in ochain.steps(wl, calib):
+        n_out, k_in = wd["w"].shape
+        say(f"{name} {key} kind={kind} m={wl.m} n={n_out} k={k_in}: every row, block layout")
+        pw = hip.PackedWeight.pack(wd["w"], wd["sw"], wd["b"])
+        xd = _to_dev(hip, hip.to_t16x32(x, fill=77))
+        yl = T if kind in (3, 4) else 0
+        y = pw.run(xd, sx, kind, out_scale=so, x_layout=T, y_layout=yl, m_tokens=wl.m)
+        torch.cuda.synchronize()
+        got = y.cpu().numpy()
+        del y
+        if yl == T:
+            got = hip.from_t16x32(got, wl.m, n_out)
+        check(kind, got, ref, f"{name} {key}")
+        del got
+        a = pw.run(xd, sx, 0, x_layout=T, m_tokens=wl.m)
+        torch.cuda.synchronize()
+        check(0, a.cpu().numpy(), acc, f"{name} {key} int32")
+        del a, xd
+        pw.free()
+
+
+@pytest.mark.parametrize("name", ["c1", "c2"])
+def test_chain_gpu_to_gpu(hip, name):
+    """The whole chain on the GPU: the first op's input is quantised on the
+    GPU into the block layout, and every later op reads the previous op's
+    int8 output where the GPU wrote it (nothing returns to the host between
+    ops). Each hop's input is held to the int8 bar against the oracle chain's
+    input for that op, and each hop's output to its kind's bar against the
+    oracle applied to the very input the hop consumed."""
+    import torch
+    wl = wk.workloads()[name]
+    calib = _calib()[name]
+    outs, scales, ins = ochain.run(wl, calib=calib)
+    dev = {}
+    for layer, op in wk.op_list(wl):
+        key = ochain.op_key(layer, op.name)
+        src = wl.op_src(layer, op)
+        kind = KINDS[wl.op_kind(layer, op)]
+        so = float(calib.get(key, 1.0))
+        x_ref, sx = ins[key]
+        if src == "seeded":
+            xf = (x_ref.astype(np.float32) * np.float32(sx)).astype(np.float32)
+            xd = hip.quantize_act(torch.from_numpy(xf).cuda(), sx, layout=T)
+        else:
+            xd = dev[src]
+        wd = wk.op_weight(wl, layer, op)
+        pw = hip.PackedWeight.pack(wd["w"], wd["sw"], wd["b"])
+        yl = T if kind in (3, 4) else 0
+        say(f"{name} {key} kind={kind}: input from {src} on the GPU")
+        y = pw.run(xd, sx, kind, out_scale=so, x_layout=T, y_layout=yl, m_tokens=wl.m)
+        dev[key] = y
+        torch.cuda.synchronize()
+        x_used = hip.from_t16x32(xd.cpu().numpy(), wl.m, op.k_in)
+        check(3, x_used, x_ref, f"{name} {key}: hop input vs the oracle chain")
+        got = y.cpu().numpy()
+        if yl == T:
+            got = hip.from_t16x32(got, wl.m, op.n_out)
+        ref = oracle.linear(x_used, wd["w"], sx, wd["sw"], wd["b"], kind, so=so)
+        check(kind, got, ref, f"{name} {key}: hop output")
+        pw.free()

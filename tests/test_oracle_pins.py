@@ -321,3 +321,22 @@ def test_chain_feeds_the_calibrated_output_scale_forward(monkeypatch):
     assert np.array_equal(outs["L0.a"], np.array([[127, -64, 63, 64]], np.int8))
     assert ins["L0.b"][1] == np.float32(1.0)
     assert np.array_equal(outs["L0.b"], np.array([[63.5, -32.0, 63.75, 31.5]], np.float32))
+
+
+def test_chain_steps_give_run_outputs():
+    """The streaming chain (accumulators, then the epilogue) yields exactly
+    what the whole-chain runner gives, op by op, with each op's input being
+    the previous op's int8 output."""
+    import oracle.chain as chain
+    import workloads as wk
+    wl = wk.workloads()["c3_seq128_s80"]
+    outs, scales, ins = chain.run(wl)
+    calib = dict(scales)
+    n = 0
+    for key, wd, x, sx, kind, so, acc, y in chain.steps(wl, calib):
+        xr, sxr = ins[key]
+        assert np.array_equal(x, xr) and sx == sxr
+        assert np.array_equal(acc, oracle.acc(xr, wd["w"]))
+        assert np.array_equal(y, outs[key])
+        n += 1
+    assert n == len(wk.op_list(wl)) == 24
