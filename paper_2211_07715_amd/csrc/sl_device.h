@@ -153,6 +153,13 @@ struct EpiOut<SL_EPI_F32_GELU> {
     static constexpr int kBytes = 4;
 };
 
+// 8-byte LDS read at a 32-bit LDS address
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ u32x2 lds_read_u2(uint32_t addr)
+{
+    return *(const __attribute__((address_space(3))) u32x2 *)(uintptr_t)addr;
+}
+
 // Epilogue of one accumulator group: s = input scale x weight scales, b =
 // biases of the 4 channels; tab, hinv, off, cmax (= kGeluBase + cells - 1):
 // the GELU step table.
@@ -166,18 +173,28 @@ __device__ __forceinline__ typename EpiOut<KIND>::T epilogue_value_s(float inv_s
     if constexpr (KIND == SL_EPI_ACC_I32) {
         return acc;
     } else if constexpr (KIND == SL_EPI_I8_GELU) {
+        // byte selectors of the permute that writes code r into byte r of
+        // the packed word: earlier bytes kept (4 + i), byte r taken from the
+        // cell's codes (0: q_lo, 1: q_hi), later bytes zero (0x0c)
+        constexpr uint32_t kSelLo[4] = {0x0c0c0c00u, 0x0c0c0004u, 0x0c000504u, 0x00060504u};
+        constexpr uint32_t kSelHi[4] = {0x0c0c0c01u, 0x0c0c0104u, 0x0c010504u, 0x01060504u};
+        // (read through readfirstlane: a uniform register operand of the
+        // shift-and-add, not a constant folded into two instructions)
+        const uint32_t tab_adj = (uint32_t)__builtin_amdgcn_readfirstlane(
+            (int)((uint32_t)(uintptr_t)(const __attribute__((address_space(3))) GeluCell *)tab -
+                  (__float_as_uint(kGeluBase) << 3)));
         uint32_t packed = 0;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             float y = (float)acc[r] * s[r];
             y = y + b[r];
             const float c = __builtin_amdgcn_fmed3f(__builtin_fmaf(y, hinv, off), kGeluBase, cmax);
-            // one 8-byte read: threshold, then the two codes (the cell index
-            // is the low bits of c, see kGeluBase)
-            const uint32_t ci = __float_as_uint(c) - __float_as_uint(kGeluBase);
-            const uint2 cell = *reinterpret_cast<const uint2 *>(reinterpret_cast<const char *>(tab) + ci * 8u);
-            const uint32_t q = y >= __uint_as_float(cell.x) ? cell.y >> 8 : cell.y;
-            packed |= (q & 0xffu) << (8 * r);
+            // one 8-byte read: threshold, then the two codes. The bits of c
+            // are those of kGeluBase plus the cell index (see kGeluBase), so
+            // one shift-and-add with tab_adj = (LDS address of the table) -
+            // 8 * bits(kGeluBase), modulo 2^32, gives the cell's address.
+            const u32x2 cell = lds_read_u2((__float_as_uint(c) << 3) + tab_adj);
+            packed = __builtin_amdgcn_perm(packed, cell.y, y >= __uint_as_float(cell.x) ? kSelHi[r] : kSelLo[r]);
         }
         return packed;
     } else {
