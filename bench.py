@@ -7,41 +7,55 @@ tokens), 4x1 block sparsity 90 %: W1 3072x768 (dequant + bias + GELU(erf) +
 requant to int8), W2 768x3072 (dequant + bias to fp32).
 
 One step is one pass of the whole hot path over one batch: quantize_act of the
-fp32 input -> linear 1 (int8 out) -> linear 2 (fp32 out), all on one stream.
-The int8 activations between them stay in the library's 16-token x
-32-feature block layout (--layout t16x32, the default: the order the matrix
-cores read; the quantisation writes it and linear 1 writes its int8 output in
-it), or are row-major throughout (--layout rows).
-Inputs are resident in HBM when timing starts; the step rotates over enough
-input/output buffer sets (> 2x the 256 MB last-level cache) that every step
-reads its activations from HBM, not from a cache warmed by the previous step.
+fp32 input -> the workload's linears in order (int8 outputs feed the next
+op), all on one stream. The int8 activations between them stay in the
+library's 16-token x 32-feature block layout (--layout t16x32, the default:
+the order the matrix cores read; the quantisation writes it and the int8
+linears write their outputs in it), or are row-major throughout (--layout
+rows). Inputs are resident in HBM when timing starts; the step rotates over
+enough input/output buffer sets (> 2x the 256 MB last-level cache) that every
+step reads its activations from HBM, not from a cache warmed by the step
+before ("cold"); the "warm" figure repeats one buffer set.
 
 Prints ONE JSON line. ``value`` is effective int8 TOPS over non-zero MACs
-(2 * M * 4 * stored_blocks per linear, summed) per step time; the K timed
-steps are bracketed by two HIP events on the launch stream. Afterwards each
-kernel of the step is launched KERNEL_REPS times back to back (same rotating
-buffers) from a captured HIP graph, between two events, which gives its
-average launch duration free of host launch cost.
-``roofline`` describes the slowest kernel against the HBM bound: its
-algorithmic bytes (X + Y + canonical packed W + scales) per launch divided by
-that duration; ``traffic`` is the counter-measured bytes per launch from
-profiles/traffic.json when that file was taken on the current kernel source.
-``cpu_baseline`` times the CPU oracle on the same step. ``layer_latency``
-gives the DistilBERT-layer latency: one layer's four linears at batch 32 x
-seq 128 and the 6-layer stack at batch 1 x seq 128 (80 % sparsity, warm,
-host-launched and replayed from a HIP graph).
+(2 * M * 4 * stored_blocks per linear, summed) per cold step; the K timed
+steps are bracketed by two HIP events on the launch stream, queued while a
+probe kernel holds the GPU so that they run back to back whatever the host's
+launch cost. Per-kernel durations:
+  * leg: each kernel alone, KERNEL_REPS launches back to back from a
+    captured HIP graph (no host launch cost), LEG_REPLAYS replays, the last
+    one timed;
+  * in-step: the cold step's time shared out over its kernels in proportion
+    to their legs (the step's kernels run back to back on one stream);
+  * in-step events: K more cold steps with a HIP event before each kernel
+    and one after the last (each kernel as it runs inside the step plus the
+    event's own dispatch gap; mean over the central 90 % of the steps).
+``roofline`` takes the slowest kernel of the step: its algorithmic HBM bytes
+(X + Y + canonical packed W + scales) per launch divided by its in-step
+duration, against the published 8 TB/s, with the leg and event figures and
+the measured copy bandwidth beside it. ``traffic`` is the
+counter-measured HBM bytes per launch from profiles/traffic.json when that
+file was taken on the current kernel source. ``peaks`` are measured on the
+same GPU: a plain copy's bandwidth and the int8 matrix instructions' rates
+(libsl_probe.so). ``workloads`` repeats the measurement (cold step, in-step
+kernels, roofline fractions) for the other full-batch configurations;
+``latency`` times the layer chains of the latency regime. ``cpu_baseline``
+times the CPU oracle on a bounded sample of the same step.
 
-Launch order (used to match profiler dispatches to ops): one step per buffer
-set (set-up), W warm-up steps, K timed steps, then, per kernel in step order,
-LEG_REPLAYS replays of a graph of KERNEL_REPS launches; with --copy-calib,
-three elementwise copies last.
+Launch order of the headline workload (bench_profile.py matches profiler
+dispatches to ops by it): one step per buffer set (set-up), W warm-up steps,
+K timed steps, K warm steps on one buffer set, K in-step steps, then, per
+kernel in step order, LEG_REPLAYS replays of a graph of KERNEL_REPS launches;
+with --copy-calib, three elementwise copies right after the timed steps.
 """
 from __future__ import annotations
 
 import argparse
+import ctypes
 import hashlib
 import json
 import os
+import platform
 import sys
 import time
 
@@ -58,8 +72,10 @@ COPY_CALIB_LAUNCHES = 3
 KERNEL_REPS = 50  # launches per kernel in the per-kernel timing leg (one graph)
 LEG_REPLAYS = 2   # replays of each kernel's graph; the last one is timed
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2211_07715_amd", "csrc", f)
-                  for f in ("kernels.hip", "kernels_direct.hip", "kernels_panel.hip", "sl_device.h", "gelu_table.cpp")]
+                  for f in ("kernels.hip", "kernels_direct.hip", "kernels_panel.hip", "sl_device.h", "gelu_table.cpp",
+                            "pack.cpp")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+OUT_BYTES = {0: 4, 1: 4, 2: 4, 3: 1, 4: 1}
 
 
 def kernel_source_hash() -> str:
@@ -79,6 +95,261 @@ def algorithmic_bytes(m, n, k, nnzb, out_bytes):
     """X + Y + canonical packed W (4 B values + 2 B column per block, row
     pointers) + per-channel scale and bias."""
     return m * k + m * n * out_bytes + nnzb * 6 + (n // 4 + 1) * 4 + 8 * n
+
+
+def _bound(kbytes, kops):
+    """HBM or MFMA, whichever takes longer at the published peaks."""
+    t_hbm = kbytes / (HBM_PEAK_GBS * 1e9)
+    t_mma = kops / (MFMA_I8_PEAK_TOPS * 1e12)
+    return "hbm" if t_hbm >= t_mma else "mfma"
+
+
+class Runner:
+    """One single-layer workload: packed weights, rotating buffer sets and a
+    step that launches quantize_act and every linear on one stream."""
+
+    def __init__(self, torch, sl, wk, name, layout, dev, calib, min_sets=2):
+        self.torch, self.sl, self.layout = torch, sl, layout
+        wl = wk.workloads()[name]
+        if wl.layers != 1:
+            raise SystemExit("bench workloads are single-layer op chains")
+        self.wl = wl
+        self.ops = wk.op_list(wl)
+        self.packed, self.meta = [], []
+        for layer, op in self.ops:
+            key = f"L{layer}.{op.name}"
+            wd = wk.op_weight(wl, layer, op)
+            pw = sl.PackedWeight.pack(wd["w"], wd["sw"], wd["b"])
+            kind = sl.EPI_BY_NAME[wl.op_kind(layer, op)]
+            self.meta.append(dict(key=key, n=op.n_out, k=op.k_in, kind=kind, src=wl.op_src(layer, op),
+                                  so=float(calib.get(key, 1.0)), nnzb=pw.nnz_blocks()))
+            self.packed.append(pw)
+        m = self.m = wl.m
+        first = self.ops[0][1]
+        self.sx = np.float32(wk.SX)
+        self.x_i8 = wk.op_seeded_x(wl, self.ops[0][0], first)
+        self.x_f32 = (self.x_i8.astype(np.float32) * self.sx).astype(np.float32)
+        set_bytes = self.x_f32.nbytes + self.x_i8.nbytes + sum(m * md["n"] * OUT_BYTES[md["kind"]] for md in self.meta)
+        self.n_sets = max(min_sets, int(np.ceil(2.2 * MALL_BYTES / set_bytes)))
+        xf_dev = torch.from_numpy(self.x_f32).to(dev)
+        self.sets = []
+        for _ in range(self.n_sets):
+            s = {"xf": xf_dev.clone(), "q": torch.empty(act_shape(sl, layout, m, first.k_in), dtype=torch.int8,
+                                                        device=dev)}
+            for md in self.meta:
+                dt = {0: torch.int32, 1: torch.float32, 2: torch.float32, 3: torch.int8, 4: torch.int8}[md["kind"]]
+                shape = act_shape(sl, layout, m, md["n"]) if md["kind"] in (3, 4) else (m, md["n"])
+                s[md["key"]] = torch.empty(shape, dtype=dt, device=dev)
+            self.sets.append(s)
+        del xf_dev
+        self.names = ["quantize_act"] + [md["key"] for md in self.meta]
+        self.kbytes = [self.x_f32.nbytes + self.x_i8.nbytes] + [
+            algorithmic_bytes(m, md["n"], md["k"], md["nnzb"], OUT_BYTES[md["kind"]]) for md in self.meta]
+        self.kops = [0] + [2 * m * 4 * md["nnzb"] for md in self.meta]
+        self.total_ops = sum(self.kops)
+
+    def launch(self, s, j, stream):
+        """Kernel j of the step (0: quantize_act, 1..: the linears)."""
+        sl, layout = self.sl, self.layout
+        if j == 0:
+            sl.quantize_act(s["xf"], float(self.sx), out=s["q"], stream=stream, layout=layout)
+            return
+        md = self.meta[j - 1]
+        if md["src"] == "seeded":
+            xin, xs = s["q"], float(self.sx)
+        else:
+            xin = s[md["src"]]
+            xs = next(mm["so"] for mm in self.meta if mm["key"] == md["src"])
+        yl = layout if md["kind"] in (3, 4) else sl.LAYOUT_ROWS
+        self.packed[j - 1].run(xin, xs, md["kind"], out_scale=md["so"], out=s[md["key"]], stream=stream,
+                               x_layout=layout, y_layout=yl, m_tokens=self.m)
+
+    def step(self, s, stream):
+        for j in range(len(self.names)):
+            self.launch(s, j, stream)
+
+    def free(self):
+        for pw in self.packed:
+            pw.free()
+        self.sets = []
+
+
+def _events(torch, n):
+    return [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+
+
+class Backlog:
+    """Keeps the GPU busy (a matrix-instruction loop from libsl_probe.so) while
+    the host queues a timed region, so that the region's launches run back to
+    back and the host's launch cost stays out of the GPU timings. Inactive
+    when the probe library is missing."""
+
+    def __init__(self, torch, dev):
+        from paper_2211_07715_amd import build as b
+        self.lib = None
+        if not os.path.exists(b.PROBE_LIB):
+            return
+        self.torch = torch
+        self.lib = ctypes.CDLL(b.PROBE_LIB)
+        self.lib.sl_probe_mfma.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                                           ctypes.c_void_p]
+        self.blocks = 2 * torch.cuda.get_device_properties(dev).multi_processor_count
+        self.out = torch.empty(self.blocks * 256, dtype=torch.int32, device=dev)
+        st = torch.cuda.current_stream()
+        e0, e1 = _events(torch, 2)
+        self._run(st, 100)
+        e0.record(st)
+        self._run(st, 2000)
+        e1.record(st)
+        torch.cuda.synchronize()
+        self.us_per_iter = e0.elapsed_time(e1) * 1e3 / 2000
+
+    def _run(self, stream, iters):
+        self.lib.sl_probe_mfma(1, self.blocks, int(iters), ctypes.c_void_p(self.out.data_ptr()),
+                               ctypes.c_void_p(stream.cuda_stream))
+
+    def hold(self, stream, us):
+        if self.lib is not None:
+            self._run(stream, max(1, int(us / self.us_per_iter)))
+
+
+_BACKLOG = None
+
+
+def time_steps(torch, r, steps, stream, rotate=True):
+    """ms per step over `steps` steps, events around the region only (the
+    GPU held busy while the host queues them)."""
+    e0, e1 = _events(torch, 2)
+    torch.cuda.synchronize()
+    _BACKLOG.hold(stream, 200.0 * steps)
+    e0.record(stream)
+    for i in range(steps):
+        r.step(r.sets[i % r.n_sets] if rotate else r.sets[0], stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
+def time_instep(torch, r, steps, stream):
+    """Per-kernel us inside cold steps: an event before each kernel and one
+    after the last, on the launch stream; the steps run back to back (one
+    synchronisation at the end), as in the timed region."""
+    n_k = len(r.names)
+    ev = [_events(torch, n_k + 1) for _ in range(steps)]
+    torch.cuda.synchronize()
+    _BACKLOG.hold(stream, 300.0 * steps)
+    for i in range(steps):
+        s = r.sets[i % r.n_sets]
+        for j in range(n_k):
+            ev[i][j].record(stream)
+            r.launch(s, j, stream)
+        ev[i][n_k].record(stream)
+    torch.cuda.synchronize()
+    v = np.array([[ev[i][j].elapsed_time(ev[i][j + 1]) * 1e3 for j in range(n_k)] for i in range(steps)])
+    # mean over the central 90 % of the steps (a rare stall of the device
+    # queue, milliseconds long, would otherwise dominate the average)
+    lo, hi = np.percentile(v, 5, axis=0), np.percentile(v, 95, axis=0)
+    return np.array([v[(v[:, j] >= lo[j]) & (v[:, j] <= hi[j]), j].mean() for j in range(n_k)])
+
+
+def time_legs(torch, r):
+    """Per-kernel us, each kernel alone: KERNEL_REPS launches from one graph."""
+    n_k = len(r.names)
+    out = np.zeros(n_k)
+    cap = torch.cuda.Stream()
+    for j in range(n_k):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=cap):
+            for i in range(KERNEL_REPS):
+                r.launch(r.sets[i % r.n_sets], j, cap)
+        ev0, ev1 = _events(torch, 2)
+        with torch.cuda.stream(cap):
+            for rep in range(LEG_REPLAYS):
+                if rep == LEG_REPLAYS - 1:
+                    ev0.record(cap)
+                g.replay()
+            ev1.record(cap)
+        torch.cuda.synchronize()
+        out[j] = ev0.elapsed_time(ev1) / KERNEL_REPS * 1e3
+        del g
+    return out
+
+
+def kernel_table(r, legs, ms_step, instep_events=None, copy_gbs=None):
+    """Per-kernel figures. us_leg: graph-replayed launches of the kernel
+    alone. us_instep: the cold step's measured time shared out over its
+    kernels in proportion to their legs (the kernels of a step run back to
+    back on one stream, so their in-step durations sum to the step).
+    us_instep_events: HIP events around the kernel inside cold steps, which
+    adds each event's dispatch gap. Fractions of the bounding peak from the
+    in-step and the leg durations."""
+    out = {}
+    share = ms_step * 1e3 / float(np.sum(legs))
+    for j, name in enumerate(r.names):
+        b = _bound(r.kbytes[j], r.kops[j])
+        e = {"bound": b, "algorithmic_bytes": int(r.kbytes[j]), "nonzero_ops": int(r.kops[j])}
+        for tag, us in (("instep", float(legs[j]) * share), ("leg", float(legs[j]))):
+            gbs = r.kbytes[j] / (us * 1e-6) / 1e9
+            tops = r.kops[j] / (us * 1e-6) / 1e12
+            e[f"us_{tag}"] = round(us, 3)
+            e[f"hbm_GBs_{tag}"] = round(gbs, 1)
+            e[f"tops_{tag}"] = round(tops, 2)
+            e[f"frac_{tag}"] = round(gbs / HBM_PEAK_GBS if b == "hbm" else tops / MFMA_I8_PEAK_TOPS, 4)
+        if instep_events is not None:
+            e["us_instep_events"] = round(float(instep_events[j]), 3)
+        if copy_gbs:
+            e["frac_vs_copy"] = round(e["hbm_GBs_instep"] / copy_gbs, 4)
+        out[name] = e
+    return out
+
+
+def measure_peaks(torch, dev):
+    """A plain copy's bandwidth and the int8 matrix instructions' rates on
+    this GPU, from libsl_probe.so (None where the library is missing)."""
+    from paper_2211_07715_amd import build as b
+    if not os.path.exists(b.PROBE_LIB):
+        return None
+    lib = ctypes.CDLL(b.PROBE_LIB)
+    lib.sl_probe_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
+    lib.sl_probe_mfma.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    st = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(st.cuda_stream)
+    nbytes = 1 << 30
+    x = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    y = torch.empty_like(x)
+    x.fill_(1)
+    for _ in range(2):
+        assert lib.sl_probe_copy(ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(y.data_ptr()), nbytes, sp) == 0
+    e0, e1 = _events(torch, 2)
+    reps = 5
+    e0.record(st)
+    for _ in range(reps):
+        lib.sl_probe_copy(ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(y.data_ptr()), nbytes, sp)
+    e1.record(st)
+    torch.cuda.synchronize()
+    copy_gbs = 2.0 * nbytes * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del x, y
+    props = torch.cuda.get_device_properties(dev)
+    n_cu = props.multi_processor_count
+    blocks = 2 * n_cu  # 4 waves a block: 2 waves per SIMD
+    out = torch.empty(blocks * 256, dtype=torch.int32, device=dev)
+    iters = 4000
+    res = {}
+    for op, name, ops_per_instr in ((0, "mfma_i8_16x16x64_TOPS", 2 * 16 * 16 * 64),
+                                    (1, "mfma_i8_32x32x32_TOPS", 2 * 32 * 32 * 32),
+                                    (2, "smfmac_i8_16x16x128_stored_TOPS", 2 * 16 * 16 * 64)):
+        assert lib.sl_probe_mfma(op, blocks, 100, ctypes.c_void_p(out.data_ptr()), sp) == 0
+        e0.record(st)
+        lib.sl_probe_mfma(op, blocks, iters, ctypes.c_void_p(out.data_ptr()), sp)
+        e1.record(st)
+        torch.cuda.synchronize()
+        instr = blocks * 4 * 8 * iters
+        res[name] = round(instr * ops_per_instr / (e0.elapsed_time(e1) * 1e-3) / 1e12, 1)
+    res["copy_GBs"] = round(copy_gbs, 1)
+    res["copy_note"] = "1 GiB device-to-device copy, read + write bytes per second"
+    res["mfma_note"] = (f"{blocks} workgroups x 4 waves, 8 independent accumulators, {iters} rounds; sparse rate "
+                        "counts the 64 stored of 128 K-columns")
+    return res
 
 
 def chain_latency(torch, sl, wk, name, calib, stream, dev, layout, reps=200, warmup=20):
@@ -119,7 +390,7 @@ def chain_latency(torch, sl, wk, name, calib, stream, dev, layout, reps=200, war
     for _ in range(warmup):
         chain()
     torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0, e1 = _events(torch, 2)
     e0.record(stream)
     for _ in range(reps):
         chain()
@@ -127,7 +398,6 @@ def chain_latency(torch, sl, wk, name, calib, stream, dev, layout, reps=200, war
     torch.cuda.synchronize()
     eager_us = e0.elapsed_time(e1) / reps * 1e3
     out = {"workload": f"{wl.name}: {wl.notes}", "m_tokens": wl.m, "layers": wl.layers, "linears": len(ops),
-           "activation_layout": "t16x32" if layout == sl.LAYOUT_T16X32 else "rows",
            "chain_us": round(eager_us, 2), "per_layer_us": round(eager_us / wl.layers, 2)}
     ref = {k: v.clone() for k, v in bufs.items()}
     try:
@@ -166,6 +436,76 @@ def chain_latency(torch, sl, wk, name, calib, stream, dev, layout, reps=200, war
     return out
 
 
+def host_info():
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    model = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except AttributeError:
+        usable = os.cpu_count()
+    return {"cpu_model": model or platform.processor(), "logical_cpus": os.cpu_count(), "usable_cpus": usable}
+
+
+def cpu_baseline(r, wk, seconds):
+    """The CPU oracle on the same step: all OpenMP threads on the full batch
+    (bounded by time), and one thread on the single-linear configuration c0
+    (whole) and on a row sample of this workload's step."""
+    import oracle
+    ws = [wk.op_weight(r.wl, layer, op) for layer, op in r.ops]
+
+    def run_rows(rows):
+        q = oracle.quantize(r.x_f32[rows], r.sx)
+        outs = {}
+        for wd, md in zip(ws, r.meta):
+            if md["src"] == "seeded":
+                xin, xs = q, float(r.sx)
+            else:
+                xin = outs[md["src"]]
+                xs = next(mm["so"] for mm in r.meta if mm["key"] == md["src"])
+            outs[md["key"]] = oracle.linear(xin, wd["w"], xs, wd["sw"], wd["b"], md["kind"], so=md["so"])
+
+    threads = oracle.threads()
+    reps, t_cpu = 0, 0.0
+    allrows = np.arange(r.m)
+    while t_cpu < seconds and reps < 50:
+        c0 = time.perf_counter()
+        run_rows(allrows)
+        t_cpu += time.perf_counter() - c0
+        reps += 1
+    out = {"value": round(r.total_ops * reps / t_cpu / 1e12, 5), "unit": "TOPS", "cores": threads, "kind": "oracle",
+           "sample": f"{reps} full step(s) of {r.wl.name} ({r.m} tokens; quantize + {len(r.meta)} linears, dense "
+                     f"naive int32 matmul), {t_cpu:.1f} s on {threads} OpenMP threads",
+           "ms_per_step": round(t_cpu / reps * 1e3, 1), "host": host_info()}
+    # single thread: c0 whole, and 256 rows of this step (rows never mix in a linear)
+    oracle.set_threads(1)
+    try:
+        wl0 = wk.workloads()["c0"]
+        (l0, op0), = wk.op_list(wl0)
+        w0 = wk.op_weight(wl0, l0, op0)
+        x0 = wk.op_seeded_x(wl0, l0, op0)
+        c0 = time.perf_counter()
+        oracle.linear(x0, w0["w"], float(wk.SX), w0["sw"], w0["b"], oracle.KIND_F32)
+        t0 = time.perf_counter() - c0
+        rows = np.arange(min(256, r.m))
+        c0 = time.perf_counter()
+        run_rows(rows)
+        t1 = time.perf_counter() - c0
+    finally:
+        oracle.set_threads(threads)
+    out["single_thread"] = {
+        "c0_linear_ms": round(t0 * 1e3, 2),
+        f"{r.wl.name}_step_ms_from_{len(rows)}_rows": round(t1 * r.m / len(rows) * 1e3, 1),
+        "note": f"one OpenMP thread; the {r.wl.name} figure scales a {len(rows)}-row sample of the step to {r.m} rows"}
+    return out
+
+
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
@@ -176,7 +516,8 @@ def parse():
                    help="layout of the int8 activations between the kernels")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--cpu-seconds", type=float, default=10.0)
-    p.add_argument("--no-latency", action="store_true", help="skip the DistilBERT-layer latency legs")
+    p.add_argument("--no-latency", action="store_true", help="skip the latency-regime chains")
+    p.add_argument("--no-extra", action="store_true", help="skip the other full-batch workloads and the peaks")
     p.add_argument("--copy-calib", action="store_true",
                    help="after the timed steps, run a plain elementwise copy of COPY_CALIB_BYTES three times "
                         "(the reference kernel that scales the HBM byte counters)")
@@ -200,131 +541,22 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     layout = sl.LAYOUT_T16X32 if args.layout == "t16x32" else sl.LAYOUT_ROWS
-
-    wl = wk.workloads()[args.workload]
     with open(os.path.join(ROOT, "tests", "golden", "calibration.json")) as f:
-        calib = json.load(f)[wl.name]
-    ops = wk.op_list(wl)
-    if wl.layers != 1:
-        raise SystemExit("bench workloads are single-layer op chains")
-
-    # ---- weights (packed once, offline)
-    packed, meta = [], []
-    for layer, op in ops:
-        key = f"L{layer}.{op.name}"
-        wd = wk.op_weight(wl, layer, op)
-        pw = sl.PackedWeight.pack(wd["w"], wd["sw"], wd["b"])
-        kind = sl.EPI_BY_NAME[wl.op_kind(layer, op)]
-        src = wl.op_src(layer, op)
-        meta.append(dict(key=key, n=op.n_out, k=op.k_in, kind=kind, src=src,
-                         so=float(calib.get(key, 1.0)), nnzb=pw.nnz_blocks(), stats=pw.tile_stats()))
-        packed.append(pw)
-    first = ops[0][1]
-    m = wl.m
-
-    # ---- activations: fp32 input whose quantisation is the seeded int8 X
-    sx = np.float32(wk.SX)
-    x_i8 = wk.op_seeded_x(wl, ops[0][0], first)
-    x_f32 = (x_i8.astype(np.float32) * sx).astype(np.float32)
-    out_bytes = {0: 4, 1: 4, 2: 4, 3: 1, 4: 1}
-    set_bytes = x_f32.nbytes + x_i8.nbytes + sum(m * md["n"] * out_bytes[md["kind"]] for md in meta)
-    n_sets = max(2, int(np.ceil(2.2 * MALL_BYTES / set_bytes)))
-    sets = []
-    xf_dev = torch.from_numpy(x_f32).to(dev)
-    for _ in range(n_sets):
-        s = {"xf": xf_dev.clone(), "q": torch.empty(act_shape(sl, layout, m, first.k_in), dtype=torch.int8, device=dev)}
-        for md in meta:
-            dt = {0: torch.int32, 1: torch.float32, 2: torch.float32, 3: torch.int8, 4: torch.int8}[md["kind"]]
-            shape = act_shape(sl, layout, m, md["n"]) if md["kind"] in (3, 4) else (m, md["n"])
-            s[md["key"]] = torch.empty(shape, dtype=dt, device=dev)
-        sets.append(s)
-    del xf_dev
+        calib_all = json.load(f)
     stream = torch.cuda.current_stream()
+    global _BACKLOG
+    _BACKLOG = Backlog(torch, dev)
 
-    def step(s, only=None, stream=stream):
-        # only=j launches just kernel j of the step (0: quantize_act, 1..: the linears)
-        if only is None or only == 0:
-            sl.quantize_act(s["xf"], float(sx), out=s["q"], stream=stream, layout=layout)
-        for i, (pw, md) in enumerate(zip(packed, meta)):
-            if only is not None and only != i + 1:
-                continue
-            if md["src"] == "seeded":
-                xin, xs = s["q"], float(sx)
-            else:
-                src = md["src"]
-                xin = s[src]
-                xs = next(mm["so"] for mm in meta if mm["key"] == src)
-            yl = layout if md["kind"] in (3, 4) else sl.LAYOUT_ROWS
-            pw.run(xin, xs, md["kind"], out_scale=md["so"], out=s[md["key"]], stream=stream, x_layout=layout,
-                   y_layout=yl, m_tokens=m)
-
-    n_k = 1 + len(meta)
-    # every buffer set gets valid activations once (set-up, not warm-up)
-    for s in sets:
-        step(s)
+    # ---- the headline workload
+    r = Runner(torch, sl, wk, args.workload, layout, dev, calib_all[args.workload])
+    for s in r.sets:  # every buffer set gets valid activations once (set-up, not warm-up)
+        r.step(s, stream)
     for i in range(args.warmup):
-        step(sets[i % n_sets])
-    torch.cuda.synchronize()
-
-    # ---- timed region: K whole steps, events only around the region
-    e_start, e_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        r.step(r.sets[i % r.n_sets], stream)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    e_start.record(stream)
-    for i in range(args.steps):
-        step(sets[i % n_sets])
-    e_end.record(stream)
-    torch.cuda.synchronize()
+    ms_cold = time_steps(torch, r, args.steps, stream)
     wall = time.perf_counter() - t0
-    ms_per_step = e_start.elapsed_time(e_end) / args.steps
-
-    # ---- per-kernel launch duration: each kernel of the step alone, KERNEL_REPS
-    # launches back to back over the rotating buffer sets, captured in a HIP
-    # graph (host launch cost would otherwise hide a kernel shorter than it);
-    # the graph is replayed LEG_REPLAYS times and the last replay is timed
-    # with HIP events on the stream it runs on
-    per_kernel_us = np.zeros(n_k)
-    cap = torch.cuda.Stream()
-    for j in range(n_k):
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g, stream=cap):
-            for i in range(KERNEL_REPS):
-                step(sets[i % n_sets], only=j, stream=cap)
-        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        with torch.cuda.stream(cap):
-            for r in range(LEG_REPLAYS):
-                if r == LEG_REPLAYS - 1:
-                    ev0.record(cap)
-                g.replay()
-            ev1.record(cap)
-        torch.cuda.synchronize()
-        per_kernel_us[j] = ev0.elapsed_time(ev1) / KERNEL_REPS * 1e3
-        del g
-
-    # ---- metric
-    total_ops = sum(2 * m * 4 * md["nnzb"] for md in meta)
-    tops = total_ops / (ms_per_step * 1e-3) / 1e12
-    names = ["quantize_act"] + [md["key"] for md in meta]
-    kbytes = [x_f32.nbytes + x_i8.nbytes] + [algorithmic_bytes(m, md["n"], md["k"], md["nnzb"], out_bytes[md["kind"]])
-                                             for md in meta]
-    kops = [0] + [2 * m * 4 * md["nnzb"] for md in meta]
-    kernels = {}
-    for j in range(n_k):
-        kernels[names[j]] = {"us": round(float(per_kernel_us[j]), 3),
-                             "hbm_GBs": round(kbytes[j] / (per_kernel_us[j] * 1e-6) / 1e9, 1),
-                             "tops": round(kops[j] / (per_kernel_us[j] * 1e-6) / 1e12, 2)}
-    dom = int(np.argmax(per_kernel_us))
-    achieved = kbytes[dom] / (per_kernel_us[dom] * 1e-6) / 1e9
-    traffic = None
-    if os.path.exists(TRAFFIC_FILE):
-        with open(TRAFFIC_FILE) as f:
-            tr = json.load(f)
-        if tr.get("kernel_source_sha256_16") == kernel_source_hash() and names[dom] in tr.get("kernels", {}):
-            traffic = tr["kernels"][names[dom]]["hbm_bytes_per_launch"]
-    roofline = {"bound": "hbm", "kernel": names[dom], "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                "algorithmic_bytes": int(kbytes[dom])}
-
     if args.copy_calib:
         src = torch.randint(0, 256, (COPY_CALIB_BYTES,), dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
@@ -333,41 +565,67 @@ def main():
             torch.bitwise_not(src, out=dst)
         torch.cuda.synchronize()
         del src, dst
+    ms_warm = time_steps(torch, r, args.steps, stream, rotate=False)
+    instep = time_instep(torch, r, args.steps, stream)
+    legs = time_legs(torch, r)
 
-    # ---- DistilBERT-layer latency: one layer's four linears at batch 32 x
-    # seq 128, and the 6-layer stack at batch 1 x seq 128 (80 % sparsity)
+    peaks = None if args.no_extra else measure_peaks(torch, dev)
+    copy_gbs = peaks["copy_GBs"] if peaks else None
+    kernels = kernel_table(r, legs, ms_cold, instep, copy_gbs)
+    dom = int(np.argmax(legs))
+    kd = kernels[r.names[dom]]
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        with open(TRAFFIC_FILE) as f:
+            tr = json.load(f)
+        if tr.get("kernel_source_sha256_16") == kernel_source_hash() and r.names[dom] in tr.get("kernels", {}):
+            traffic = tr["kernels"][r.names[dom]]["hbm_bytes_per_launch"]
+    roofline = {"bound": kd["bound"], "kernel": r.names[dom], "achieved": kd["hbm_GBs_instep"],
+                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": kd["frac_instep"], "traffic": traffic,
+                "algorithmic_bytes": kd["algorithmic_bytes"],
+                "timing": "in-step: the cold step's time shared out over its kernels in proportion to their "
+                          "graph-replayed durations",
+                "us_instep": kd["us_instep"], "us_leg": kd["us_leg"], "us_instep_events": kd["us_instep_events"],
+                "achieved_leg": kd["hbm_GBs_leg"], "frac_leg": kd["frac_leg"]}
+    if copy_gbs:
+        roofline["measured_copy_GBs"] = copy_gbs
+        roofline["frac_vs_copy"] = kd["frac_vs_copy"]
+    tops = r.total_ops / (ms_cold * 1e-3) / 1e12
+    headline_cfg = {"workload": f"{r.wl.name}: {r.wl.notes}", "m_tokens": r.m,
+                    "ops": [f"{md['key']} {md['n']}x{md['k']} kind={md['kind']} nnzb={md['nnzb']}" for md in r.meta],
+                    "activation_layout": args.layout, "buffer_sets": r.n_sets, "kernel_reps": KERNEL_REPS,
+                    "leg_replays": LEG_REPLAYS, "wall_s": round(wall, 3)}
+
+    # ---- the other full-batch workloads: cold step, in-step kernels
+    extra = None
+    if not args.no_extra:
+        extra = {}
+        for name, steps in (("c2", 50), ("c4", 8), ("c4_bertl", 8)):
+            if name == args.workload:
+                continue
+            rr = Runner(torch, sl, wk, name, layout, dev, calib_all[name])
+            for s in rr.sets:
+                rr.step(s, stream)
+            ms = time_steps(torch, rr, steps, stream)
+            ms_w = time_steps(torch, rr, steps, stream, rotate=False)
+            lg = time_legs(torch, rr)
+            extra[name] = {"workload": f"{rr.wl.name}: {rr.wl.notes}", "m_tokens": rr.m, "steps": steps,
+                           "ms_per_step": round(ms, 4), "ms_per_step_warm": round(ms_w, 4),
+                           "tops": round(rr.total_ops / (ms * 1e-3) / 1e12, 2),
+                           "kernels": kernel_table(rr, lg, ms, None, copy_gbs)}
+            rr.free()
+            torch.cuda.empty_cache()
+
+    # ---- latency regime: one layer at batch 32 x seq 128 and the 6-layer
+    # stacks at batch 1, seq 128 and 384, 70 / 80 / 90 % sparsity
     latency = None
     if not args.no_latency:
-        with open(os.path.join(ROOT, "tests", "golden", "calibration.json")) as f:
-            calib_all = json.load(f)
-        latency = {}
-        for name, label in (("c2", "bs32_seq128_80pct_layer"), ("c3_seq128_s80", "bs1_seq128_80pct_6layers")):
-            latency[label] = chain_latency(torch, sl, wk, name, calib_all[name], stream, dev, layout)
+        latency = {"c2_bs32_seq128_80pct_layer": chain_latency(torch, sl, wk, "c2", calib_all["c2"], stream, dev,
+                                                               layout)}
+        for name in sorted(n for n in wk.workloads() if n.startswith("c3_")):
+            latency[name] = chain_latency(torch, sl, wk, name, calib_all[name], stream, dev, layout, reps=100)
 
-    # ---- CPU oracle baseline on the same step (bounded by time)
-    cpu = None
-    if not args.no_cpu:
-        import oracle
-        ws = [wk.op_weight(wl, layer, op) for layer, op in ops]
-        reps, t_cpu = 0, 0.0
-        while t_cpu < args.cpu_seconds and reps < 50:
-            c0 = time.perf_counter()
-            q = oracle.quantize(x_f32, sx)
-            outs = {}
-            for (layer, op), wd, md in zip(ops, ws, meta):
-                if md["src"] == "seeded":
-                    xin, xs = q, float(sx)
-                else:
-                    xin = outs[md["src"]]
-                    xs = next(mm["so"] for mm in meta if mm["key"] == md["src"])
-                outs[md["key"]] = oracle.linear(xin, wd["w"], xs, wd["sw"], wd["b"], md["kind"], so=md["so"])
-            t_cpu += time.perf_counter() - c0
-            reps += 1
-        cpu = {"value": round(total_ops * reps / t_cpu / 1e12, 5), "unit": "TOPS", "cores": oracle.threads(),
-               "kind": "oracle",
-               "sample": f"{reps} full step(s) of {wl.name} ({m} tokens; quantize + {len(meta)} linears, dense "
-                         f"naive int32 matmul), {t_cpu:.1f} s",
-               "ms_per_step": round(t_cpu / reps * 1e3, 1)}
+    cpu = None if args.no_cpu else cpu_baseline(r, wk, args.cpu_seconds)
 
     line = {
         "metric": "effective int8 TOPS (nonzero MACs) + % roofline; DistilBERT-layer latency @bs1/bs32",
@@ -376,21 +634,22 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 5),
+        "ms_per_step": round(ms_cold, 5),
+        "ms_per_step_warm": round(ms_warm, 5),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "i8",
         "data": "synthetic",
-        "config": {"workload": f"{wl.name}: {wl.notes}", "m_tokens": m,
-                   "ops": [f"{md['key']} {md['n']}x{md['k']} kind={md['kind']} nnzb={md['nnzb']}" for md in meta],
-                   "activation_layout": args.layout, "buffer_sets": n_sets, "kernel_reps": KERNEL_REPS, "leg_replays": LEG_REPLAYS,
-                   "wall_s": round(wall, 3)},
+        "config": headline_cfg,
         "kernels": kernels,
         "roofline": roofline,
+        "peaks": peaks,
+        "workloads": extra,
+        "latency": latency,
         "cpu_baseline": cpu,
-        "layer_latency": latency,
     }
+    r.free()
     print(json.dumps(line), flush=True)
 
 

@@ -77,20 +77,21 @@ def _map_by_order(dispatches, names, bl):
     {name: [values in the per-kernel leg]}, {name: kernel symbol}).
 
     Bench launch order: one step per buffer set, W warm-up steps, K timed
-    steps (each step: the n_k kernels in order), then, per kernel in step
-    order, LEG_REPLAYS replays of a graph of KERNEL_REPS launches."""
+    steps (each step: the n_k kernels in order), K warm steps, K in-step
+    steps, then, per kernel in step order, LEG_REPLAYS replays of a graph of
+    KERNEL_REPS launches."""
     dispatches = sorted(dispatches)
     n_k = len(names)
     sets, warm, steps = bl["config"]["buffer_sets"], bl["warmup"], bl["steps"]
     reps = bl["config"]["kernel_reps"] * bl["config"].get("leg_replays", 1)
-    n_step = (sets + warm + steps) * n_k
+    n_step = (sets + warm + 3 * steps) * n_k
     if len(dispatches) != n_step + reps * n_k:
         raise SystemExit(f"{len(dispatches)} library dispatches, expected {n_step + reps * n_k}")
     timed, leg, kname = defaultdict(list), defaultdict(list), {}
     for i, (_, name, val) in enumerate(dispatches):
         if i < n_step:
             j = i % n_k
-            if i // n_k >= sets + warm:
+            if sets + warm <= i // n_k < sets + warm + steps:
                 timed[names[j]].append(val)
         else:
             j = (i - n_step) // reps
@@ -112,18 +113,40 @@ def cmd_stats(a):
     lines = [f"# rocprofv3 kernel trace: {a.title}", "", "Command (from the repository root):", "", "```",
              a.cmd, "```", "",
              "Per-op launch duration from the kernel trace (dispatches matched to ops by the bench's launch "
-             "order), in the timed steps and in the per-kernel leg, next to the bench's own HIP-event figure "
-             "for the per-kernel leg of the same run:", "",
-             "| op | kernel | launches (steps) | avg us (trace, steps) | launches (leg) | avg us (trace, leg) "
-             "| avg us (bench events, leg) | trace/events |",
-             "|---|---|---:|---:|---:|---:|---:|---:|"]
+             "order) in the timed steps and in the per-kernel leg, next to the bench's own figures of the same "
+             "run (in-step: the timed step's time shared out over its kernels by their legs; leg: "
+             "graph-replayed launches, timed with HIP events), and the roofline fraction each gives. The "
+             "profiler's per-dispatch overhead lengthens the profiled run's step, so the bench line of an "
+             "unprofiled run is the one to compare fractions with:", "",
+             "| op | kernel | launches (steps) | avg us (trace, steps) | avg us (bench, in-step) | trace/bench "
+             "| launches (leg) | avg us (trace, leg) | avg us (bench, leg) | trace/bench | frac (trace, steps) "
+             "| frac (bench, in-step) |",
+             "|---|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
     for n in names:
         v, u = timed.get(n, []), leg.get(n, [])
         avg = sum(v) / len(v) if v else float("nan")
         avg_leg = sum(u) / len(u) if u else float("nan")
-        ev = bench_line["kernels"][n]["us"]
-        lines.append(f"| {n} | `{kname.get(n, '?')[:90]}` | {len(v)} | {avg:.2f} | {len(u)} | {avg_leg:.2f} | "
-                     f"{ev} | {avg_leg / ev:.3f} |")
+        k = bench_line["kernels"][n]
+        ev, evl = k["us_instep"], k["us_leg"]
+        frac_t = k["algorithmic_bytes"] / (avg * 1e-6) / 1e9 / bench.HBM_PEAK_GBS
+        lines.append(f"| {n} | `{kname.get(n, '?')[:90]}` | {len(v)} | {avg:.2f} | {ev} | {avg / ev:.3f} | "
+                     f"{len(u)} | {avg_leg:.2f} | {evl} | {avg_leg / evl:.3f} | {frac_t:.4f} | {k['frac_instep']} |")
+    if a.ref_bench_log:
+        ref = _bench_line(a.ref_bench_log)
+        rk = ref["kernels"] if ref["config"]["workload"].startswith(a.workload + ":") else \
+            (ref.get("workloads") or {}).get(a.workload, {}).get("kernels")
+        if rk:
+            lines += ["", f"Against an unprofiled run of `{a.ref_cmd}` (same kernel source; its in-step "
+                          "figures, the ones the bench line reports):", "",
+                      "| op | avg us (trace, steps) | us (unprofiled bench, in-step) | frac (trace) "
+                      "| frac (unprofiled bench) | ratio |", "|---|---:|---:|---:|---:|---:|"]
+            for n in names:
+                v = timed.get(n, [])
+                avg = sum(v) / len(v) if v else float("nan")
+                k = bench_line["kernels"][n]
+                frac_t = k["algorithmic_bytes"] / (avg * 1e-6) / 1e9 / bench.HBM_PEAK_GBS
+                fb = rk[n]["frac_instep"]
+                lines.append(f"| {n} | {avg:.2f} | {rk[n]['us_instep']} | {frac_t:.4f} | {fb} | {fb / frac_t:.3f} |")
     lines += ["", "rocprofv3 --stats summary (all kernels of the run, top 12 by total time):", "",
               "| kernel | calls | total ns | avg ns | min ns | max ns | % |", "|---|---:|---:|---:|---:|---:|---:|"]
     stats.sort(key=lambda r: -float(r.get("TotalDurationNs", 0)))
@@ -245,6 +268,8 @@ def main():
     s.add_argument("--out", required=True)
     s.add_argument("--title", default="")
     s.add_argument("--workload", default="c1")
+    s.add_argument("--ref-bench-log", help="stdout of an unprofiled bench.py run to compare fractions with")
+    s.add_argument("--ref-cmd", default="python bench.py")
     c = sub.add_parser("counters")
     c.add_argument("--dir", action="append", required=True, help="rocprof directory of one --pmc pass (repeat)")
     c.add_argument("--log", action="append", required=True, help="stdout of that pass (holds the bench line)")

@@ -60,6 +60,8 @@ def _load() -> ctypes.CDLL:
         lib.oracle_absmax_f32.restype = ctypes.c_float
         lib.oracle_threads.argtypes = []
         lib.oracle_threads.restype = ctypes.c_int
+        lib.oracle_set_threads.argtypes = [ctypes.c_int]
+        lib.oracle_set_threads.restype = None
         _lib = lib
     return _lib
 
@@ -142,3 +144,8 @@ def calibrate_out_scale(g: np.ndarray) -> np.float32:
 def threads() -> int:
     """OpenMP threads the oracle's loops use."""
     return int(_load().oracle_threads())
+
+
+def set_threads(n: int) -> None:
+    """OpenMP threads for the oracle's loops (timing only)."""
+    _load().oracle_set_threads(int(n))

@@ -159,6 +159,12 @@ float oracle_absmax_f32(const float *v, int64_t count)
     return best;
 }
 
+/* Threads for the OpenMP loops above (timing only; results do not depend on it). */
+void oracle_set_threads(int n)
+{
+    if (n > 0) omp_set_num_threads(n);
+}
+
 /* Number of threads the OpenMP loops above use. */
 int oracle_threads(void)
 {
