@@ -72,8 +72,8 @@ COPY_CALIB_LAUNCHES = 3
 KERNEL_REPS = 50  # launches per kernel in the per-kernel timing leg (one graph)
 LEG_REPLAYS = 2   # replays of each kernel's graph; the last one is timed
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2211_07715_amd", "csrc", f)
-                  for f in ("kernels.hip", "kernels_direct.hip", "kernels_panel.hip", "sl_device.h", "gelu_table.cpp",
-                            "pack.cpp")]
+                  for f in ("kernels.hip", "kernels_direct.hip", "kernels_panel.hip", "kernels_split.hip", "sl_device.h",
+                            "gelu_table.cpp", "pack.cpp")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 OUT_BYTES = {0: 4, 1: 4, 2: 4, 3: 1, 4: 1}
 

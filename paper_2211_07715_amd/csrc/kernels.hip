@@ -755,6 +755,19 @@ sl_status upload_image(sl_packed_weight *w)
         set_error("packed weight image over 2 GiB (n_out x k_in too large for one image)");
         return SL_ERR_UNSUPPORTED;
     }
+    // the split-reduction kernel's overflow image (the same size as the main
+    // image, which is known to fit one buffer)
+    std::vector<int8_t> odense(ti.main.size(), 0);
+    {
+        const size_t pstride = (size_t)ti.n_tiles + 1;
+        for (int wi = 0; wi < ti.n_win; ++wi)
+            for (int t = 0; t < ti.n_tiles; ++t) {
+                const uint32_t *pp = ti.ovf_ptr.data() + (size_t)wi * pstride + t;
+                if (pp[1] > pp[0])
+                    memcpy(odense.data() + ((size_t)wi * ti.n_tiles + t) * kOpBytes,
+                           ti.ovf.data() + (size_t)pp[0] * kOpBytes, kOpBytes);
+            }
+    }
     const size_t b_main = std::max<size_t>(ti.main.size(), 16);
     const size_t b_ovf = std::max<size_t>(ti.ovf.size(), 16);
     const size_t b_vec = (size_t)w->n_out * sizeof(float);
@@ -777,6 +790,8 @@ sl_status upload_image(sl_packed_weight *w)
     o_end = align256(o_end + std::max<size_t>(ti.res_ovf.size(), 16));
     const size_t o_rdir = o_end;
     o_end = align256(o_end + std::max<size_t>(ti.res_dir.size() * sizeof(uint32_t), 16));
+    const size_t o_ovfd = o_end;
+    o_end = align256(o_end + b_main);
     const size_t total = o_end;
     void *base = nullptr;
     hipError_t e = hipMalloc(&base, total);
@@ -814,6 +829,9 @@ sl_status upload_image(sl_packed_weight *w)
     w->dev.rovf_bytes = (uint32_t)ti.res_ovf.size();
     w->dev.rdir = reinterpret_cast<const uint32_t *>(p + o_rdir);
     w->dev.res_lds_ovf = res_lds_ovf;
+    if (!odense.empty()) HIP_TRY(hipMemcpy(p + o_ovfd, odense.data(), odense.size(), hipMemcpyHostToDevice));
+    w->dev.ovfd = reinterpret_cast<const int8_t *>(p + o_ovfd);
+    w->dev.ovfd_bytes = (uint32_t)odense.size();
     w->dev.main = reinterpret_cast<const int8_t *>(p + o_main);
     w->dev.ovf = reinterpret_cast<const int8_t *>(p + o_ovf);
     w->dev.ovf_ptr = nullptr;
@@ -1141,6 +1159,7 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int32_t x_la
     a.pan_instr = 0;
     a.n_slices = 0;
     a.slice_groups = 0;
+    a.kw = 0;
     hipStream_t s = static_cast<hipStream_t>(stream);
 
     // (host stack only: the step table is copied out of a fixed-size cache)
@@ -1180,7 +1199,30 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int32_t x_la
         // block-layout output from aligned rows) or the staged kernel
         // (row-major input and output). SL_PATH=panel|direct|staged forces a
         // kernel (tests, tuning; panel falls back when no panel fits).
+        // Before all of them, few tokens (at most kSplitAutoItems work items
+        // of the split-reduction kernel, about five per compute unit) go to
+        // that kernel (SL_PATH=split forces it): there the other kernels'
+        // work items would not fill the chip and each walks its whole
+        // reduction in series.
         const char *path = env_cfg().path;
+        const bool force_split = strcmp(path, "split") == 0;
+        const int split_wpw = split_windows_per_wave(ti.n_win);
+        const int64_t split_items =
+            (a.m + 16 * kSplitSt - 1) / (16 * kSplitSt) * ((ti.n_tiles + kSplitNt - 1) / kSplitNt);
+        if (vec && (force_split || (!*path && split_items <= kSplitAutoItems)) && split_wpw > 0) {
+            a.n_cgroups = (ti.n_tiles + kSplitNt - 1) / kSplitNt;
+            a.om = nullptr;
+            a.ovf = w->dev.ovfd;  // (restored below for the other kernels' chunks)
+            a.ovf_bytes = w->dev.ovfd_bytes;
+            a.n_items = split_items;
+            a.kw = (ti.n_win + split_wpw - 1) / split_wpw;
+            const sl_status sst = launch_split(a, run_kind == SL_EPI_I8_GELU ? &ga : nullptr, run_kind, xt, yt, s);
+            if (sst != SL_OK) return sst;
+            set_last_path("split %d,%d kw=%d wpw=%d", kSplitSt, kSplitNt, a.kw, split_wpw);
+            a.ovf = w->dev.ovf;
+            a.ovf_bytes = (uint32_t)ti.ovf.size();
+            continue;
+        }
         if (vec && strcmp(path, "resident") == 0) {
             sl_status rst = try_resident(w, a, xt, yt, run_kind, run_kind == SL_EPI_I8_GELU ? &ga : nullptr, s);
             if (rst == SL_OK) continue;

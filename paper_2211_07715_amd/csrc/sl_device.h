@@ -80,6 +80,8 @@ struct LinearArgs {
     int32_t pan_instr;      // 1024-byte copies per channel group
     int32_t n_slices;       // token slices per channel group
     int32_t slice_groups;   // token groups (16 ST tokens) per slice
+    // split-reduction kernel only: waves per workgroup
+    int32_t kw;
 };
 
 // Byte offset of element (t, c) of an int8 tensor in SL_LAYOUT_T16X32 with
@@ -321,6 +323,21 @@ extern const DirectCfg kDirectCfgs[kNumDirectCfgs];
 // SL_EPI_I8_GELU; xt / yt: x / y in SL_LAYOUT_T16X32 (yt for int8 kinds)
 sl_status launch_direct(const LinearArgs &a, const GeluArg *ep, int32_t run_kind, DirectCfg c, bool xt, bool yt,
                         hipStream_t stream);
+
+// Split-reduction kernel (kernels_split.hip): one work item of kSplitSt
+// 16-token subtiles x kSplitNt 16-channel tiles per workgroup of a.kw waves
+// (1 <= kw <= kSplitMaxWaves), whose waves split the item's windows, at most
+// split_windows_per_wave(n_win) each (1 or 2: the fewer that lets
+// kSplitMaxWaves waves cover the windows; 0: too many windows, over 32, for
+// this kernel). For few tokens; aligned or block-layout token rows.
+constexpr int kSplitSt = 1;
+constexpr int kSplitNt = 2;
+constexpr int kSplitWin = 2;
+constexpr int kSplitMaxWaves = 16;
+constexpr int64_t kSplitAutoItems = 1280;  // automatic choice up to this many work items
+int split_windows_per_wave(int32_t n_win);
+sl_status launch_split(const LinearArgs &a, const GeluArg *ep, int32_t run_kind, bool xt, bool yt,
+                       hipStream_t stream);
 
 // Workgroup shapes of the weight-stationary kernel (kernels_panel.hip): NWV
 // waves, each multiplying ST 16-token subtiles by the NT 16-channel tiles of

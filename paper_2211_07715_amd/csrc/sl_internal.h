@@ -147,6 +147,10 @@ struct DeviceImage {
     // one workgroup's operands take, rounded up to whole 1024-byte copies
     const int8_t *rovf = nullptr;
     uint32_t rovf_bytes = 0;
+    // split-reduction kernel: the overflow operands in the main image's
+    // order, one slot per (window, tile), zeros where the tile has none
+    const int8_t *ovfd = nullptr;
+    uint32_t ovfd_bytes = 0;
     const uint32_t *rdir = nullptr;
     uint32_t res_lds_ovf = 0;
     int64_t bytes = 0;
@@ -184,7 +188,7 @@ void clear_error();
 // Kernel-choice overrides for tests and tuning (SL_PATH, SL_TILE, SL_DTILE,
 // SL_PTILE), read from the environment once and again on sl_reload_env()
 struct EnvCfg {
-    char path[16];  // "" (automatic), "panel", "direct", "staged", "resident"
+    char path[16];  // "" (automatic), "panel", "direct", "staged", "resident", "split"
     int tile[5];    // SL_TILE "st,ct,wm,wn,d"; tile[0] == 0: unset
     int dtile[4];   // SL_DTILE "st,nt,wm,d"
     int ptile[4];   // SL_PTILE "nt,st,nwv,r"

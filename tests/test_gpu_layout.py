@@ -88,6 +88,7 @@ def test_block_layout_all_kinds(hip, m, n, k, x_layout, y_layout):
 @pytest.mark.parametrize("dtile", ["2,6,4,4", "1,6,4,6", "1,2,4,8"])
 def test_block_layout_each_shape(hip, monkeypatch, dtile):
     import torch
+    monkeypatch.setenv("SL_PATH", "direct")
     monkeypatch.setenv("SL_DTILE", dtile)
     for (m, n, k) in [(77, 96, 768), (300, 200, 1000), (16, 3072, 768)]:
         w, sw, b, rng = _case(n, k, 0.15, m + n + k)

@@ -103,10 +103,12 @@ def test_panel_runs_at_distilbert_ffn_shapes(hip, monkeypatch):
 
 
 def test_default_path_choice(hip, monkeypatch):
-    """Without SL_PATH the weight-stationary kernel runs for short reductions
-    (K <= 1024) of widening layers (DistilBERT QKV and FFN1, any token count)
-    or of long token slices, and the direct kernel elsewhere: FFN2 (K = 3072)
-    and the square attention-output layer at few tokens."""
+    """Without SL_PATH few tokens (at most 1280 work items of 16 tokens x 32
+    channels) go to the split-reduction kernel; beyond that the
+    weight-stationary kernel runs for short reductions (K <= 1024) of
+    widening layers (DistilBERT QKV and FFN1) or of long token slices, and
+    the direct kernel elsewhere: FFN2 (K = 3072) and the square
+    attention-output layer."""
     import torch
     import workloads as wk
     monkeypatch.delenv("SL_PATH", raising=False)
@@ -114,7 +116,8 @@ def test_default_path_choice(hip, monkeypatch):
     for (n, k, m, s, want) in [(3072, 768, 4096, 0.9, "panel 6,2,8,2"), (3072, 768, 4096, 0.8, "panel 6,2,8,2"),
                                (3072, 768, 16384, 0.8, "panel 6,2,8,2"), (2304, 768, 384, 0.8, "panel"),
                                (768, 3072, 4096, 0.9, "direct"), (768, 768, 4096, 0.8, "direct"),
-                               (768, 768, 128, 0.9, "direct")]:
+                               (768, 768, 128, 0.9, "split"), (3072, 768, 128, 0.8, "split"),
+                               (768, 3072, 384, 0.8, "split"), (768, 768, 1024, 0.8, "direct")]:
         wd = wk.make_weight(n, k, s, seed=3)
         x = wk.make_x(m, k, seed=3)
         pw = hip.PackedWeight.pack(wd["w"], wd["sw"], wd["b"])

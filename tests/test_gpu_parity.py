@@ -65,14 +65,16 @@ def _case(n, k, density, seed):
 
 
 SMALL = [(1, 4, 1), (3, 16, 7), (16, 16, 64), (17, 20, 100), (64, 48, 768), (65, 768, 768), (200, 64, 1025),
-         (33, 32, 3072), (130, 1024, 4096), (5, 12, 2049)]
+         (33, 32, 3072), (130, 1024, 4096), (5, 12, 2049), (40, 72, 64)]
 
 
-# kernel paths: the default choice (the weight-stationary kernel where it
-# pays, else the staged kernel for row-major token rows), the staged kernel
-# forced, and the direct-operand kernel in each of its workgroup shapes (the
-# weight-stationary shapes are covered in test_gpu_panel.py)
-PATHS = {"default": {}, "staged": {"SL_PATH": "staged"}, "direct": {"SL_PATH": "direct"},
+# kernel paths: the default choice (the split-reduction kernel for few
+# aligned token rows, the weight-stationary kernel where it pays, else the
+# staged kernel for row-major token rows), the staged and the split-reduction
+# kernels forced, and the direct-operand kernel in each of its workgroup
+# shapes (the weight-stationary shapes are covered in test_gpu_panel.py)
+PATHS = {"default": {}, "staged": {"SL_PATH": "staged"}, "split": {"SL_PATH": "split"},
+         "direct": {"SL_PATH": "direct"},
          "direct_64x96": {"SL_PATH": "direct", "SL_DTILE": "1,6,4,6"},
          "direct_64x32": {"SL_PATH": "direct", "SL_DTILE": "1,2,4,8"},
          "direct_128x96": {"SL_PATH": "direct", "SL_DTILE": "2,6,4,4"}}
@@ -98,6 +100,8 @@ def test_small_shapes_all_kinds(hip, monkeypatch, m, n, k, density, path):
         ref = oracle.linear(x, w, 0.02, sw, b, kind, so=so)
         got = run_gpu(hip, pw, x, 0.02, kind, so)
         check(kind, got, ref, f"{name} m={m} n={n} k={k} d={density}")
+        if path == "split" and k % 16 == 0:
+            assert hip.last_path().startswith("split"), hip.last_path()
     pw.free()
 
 

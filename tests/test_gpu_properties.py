@@ -3,7 +3,7 @@ kernels and activation layouts, the int32 accumulators of the HIP path are
 bit-identical to the oracle's, and the fp32 outputs meet the fp32 bar.
 
 Shapes span several tiles with ragged token, channel and column tails; k is
-a multiple of 16 so that every kernel (staged, direct, weight-stationary)
+a multiple of 16 so that every kernel (staged, direct, weight-stationary, split)
 accepts row-major rows. The kernel that ran is recorded in the failure text.
 """
 import numpy as np
@@ -16,13 +16,13 @@ from test_gpu_parity import check
 
 pytestmark = pytest.mark.gpu
 
-PATHS = [{}, {"SL_PATH": "staged"}, {"SL_PATH": "direct"}, {"SL_PATH": "panel"}]
+PATHS = [{}, {"SL_PATH": "staged"}, {"SL_PATH": "direct"}, {"SL_PATH": "panel"}, {"SL_PATH": "split"}]
 
 
 @settings(max_examples=40, deadline=None, derandomize=True,
           suppress_health_check=[HealthCheck.too_slow, HealthCheck.function_scoped_fixture])
 @given(m=st.integers(1, 90), n4=st.integers(1, 48), k16=st.integers(1, 48),
-       density=st.sampled_from([0.0, 0.05, 0.2, 0.5, 1.0]), path=st.integers(0, 3),
+       density=st.sampled_from([0.0, 0.05, 0.2, 0.5, 1.0]), path=st.integers(0, len(PATHS) - 1),
        block_x=st.booleans(), seed=st.integers(0, 2 ** 31 - 1))
 def test_gpu_int32_and_fp32_match_oracle(hip, monkeypatch, m, n4, k16, density, path, block_x, seed):
     import torch
