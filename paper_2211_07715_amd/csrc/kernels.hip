@@ -701,7 +701,7 @@ sl_status upload_image(sl_packed_weight *w)
                 e[0] = mask;
                 e[1] = pp[0];
                 e[2] = (uint32_t)std::min<uint64_t>(base, UINT32_MAX);
-                base += (uint64_t)(nt + __builtin_popcount(mask)) * kOpPieces;
+                base += (uint64_t)(2 * nt) * kOpPieces;
             }
             pt[((size_t)g * (ti.n_win + 1) + ti.n_win) * 4 + 2] = (uint32_t)std::min<uint64_t>(base, UINT32_MAX);
             pan_max[i] = (uint32_t)std::min<uint64_t>(std::max<uint64_t>(pan_max[i], base), UINT32_MAX);
@@ -709,8 +709,9 @@ sl_status upload_image(sl_packed_weight *w)
     }
     // The panel images: per channel group, its window table and then its
     // panel (per window: the NT main operands, zeros past the last tile, then
-    // the window's overflow operands), padded to a common stride of whole
-    // 1024-byte copies, so that a workgroup's copies need no table read first.
+    // NT overflow operand slots, zeros where a tile has none), padded to a
+    // common stride of whole 1024-byte copies, so that a workgroup's copies
+    // need no table read first and its kernel none at all.
     // Only sizes whose panels can fit in LDS get an image.
     std::vector<std::vector<int8_t>> pimgs(pnts.size());
     std::vector<uint32_t> pstrides(pnts.size(), 0);
@@ -732,10 +733,15 @@ sl_status upload_image(sl_packed_weight *w)
             for (int wi = 0; wi < ti.n_win; ++wi) {
                 int8_t *const wb = gb + tab + (size_t)ge[wi * 4 + 2] * 16;
                 memcpy(wb, ti.main.data() + ((size_t)wi * ti.n_tiles + t0) * kOpBytes, (size_t)ntl * kOpBytes);
-                const uint32_t n_ovf = (uint32_t)__builtin_popcount(ge[wi * 4]);
-                if (n_ovf)
-                    memcpy(wb + (size_t)nt * kOpBytes, ti.ovf.data() + (size_t)ge[wi * 4 + 1] * kOpBytes,
-                                (size_t)n_ovf * kOpBytes);
+                // (the window's overflow operands are stored in tile order
+                // from entry word 1 on)
+                uint32_t rank = 0;
+                for (int j = 0; j < ntl; ++j)
+                    if ((ge[wi * 4] >> j) & 1u) {
+                        memcpy(wb + (size_t)(nt + j) * kOpBytes,
+                               ti.ovf.data() + (size_t)(ge[wi * 4 + 1] + rank) * kOpBytes, kOpBytes);
+                        ++rank;
+                    }
             }
         }
     }

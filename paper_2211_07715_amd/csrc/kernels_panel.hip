@@ -9,13 +9,15 @@
 // accumulation, one fused epilogue per output after the whole reduction).
 // What differs is the schedule. A workgroup owns one channel group (NT
 // 16-channel tiles) and one slice of the tokens. It copies the group's window
-// table and whole panel -- every window's NT main operands and the overflow
-// operands the window holds, packed, laid out that way by the packer -- into
-// LDS once, with no dependent read before the copies, then its waves work
-// through the slice's token groups on their own: a wave loads its token rows
-// (the B operands) straight into registers, R - 1 windows ahead, reads the weight
-// operands from the resident panel, and multiplies an overflow operand only
-// where the window's mask says it exists. Past the one barrier that follows
+// table and whole panel -- every window's NT main operands and NT overflow
+// operand slots (zeros where a tile has none in the window), laid out that
+// way by the packer -- into LDS once, with no dependent read before the
+// copies, then its waves work through the slice's token groups on their own:
+// a wave loads its token rows (the B operands) straight into registers,
+// R - 1 windows ahead, reads the weight operands from the resident panel at
+// offsets that follow from the window alone, and multiplies every slot, so
+// that no per-tile branch or table read sits in the loop (an absent overflow
+// operand is zeros: its products are zero). Past the one barrier that follows
 // the panel copy and the set-up there is none, so one wave's epilogue
 // overlaps the matrix instructions of the others, and the weight image is read from memory once per workgroup rather
 // than once per token tile.
@@ -98,7 +100,6 @@ __device__ __forceinline__ void panel_body(const LinearArgs &a, const GeluArg *e
     float *const vec = reinterpret_cast<float *>(smem);
     GeluCell *const tab = reinterpret_cast<GeluCell *>(smem + S::VEC);
     int8_t *const trans = smem + S::VEC + L::kTab + wave * S::TR;
-    uint4 *const wtab = reinterpret_cast<uint4 *>(smem + L::kFixed);
     int8_t *const panel = smem + L::kFixed + (a.n_win + 1) * 16;
 
     // ---- the group's window table and panel: one stride of the panel image,
@@ -167,11 +168,10 @@ __device__ __forceinline__ void panel_body(const LinearArgs &a, const GeluArg *e
     i32x8 bv[R][ST];
     static_assert(R >= 2, "at least one window loads while another is multiplied");
 
-    // Weight operands of one element in registers: the NT main operands with
-    // their index words and the overflow operands present in the element's
-    // window (the slots of absent ones keep stale values and are never
-    // multiplied). Two sets alternate: element e+1's operands are read from
-    // the panel while element e's matrix instructions run.
+    // Weight operands of one element in registers: the NT main operands and
+    // the NT overflow operand slots with their index words. Two sets
+    // alternate: element e+1's operands are read from the panel while
+    // element e's matrix instructions run.
     struct Ops {
         i32x4 av[NT], ao[NT];
         int ix[NT], io[NT];
@@ -186,22 +186,19 @@ __device__ __forceinline__ void panel_body(const LinearArgs &a, const GeluArg *e
             o.ix[c] = *reinterpret_cast<const int *>(wb + c * kOpBytes + 1024 + iword * 4);
         }
     };
-    // overflow operands present in the element (mask: their tiles)
-    auto read_ovf = [&](Ops &o, uint32_t base, uint32_t mask) {
-        const int8_t *oo = panel + base + NT * kOpBytes;
+    // overflow operand slots of the element
+    auto read_ovf = [&](Ops &o, uint32_t base) {
+        const int8_t *const oo = panel + base + NT * kOpBytes;
 #pragma unroll
         for (int c = 0; c < NT; ++c) {
-            if ((mask >> c) & 1u) {
-                o.ao[c] = *reinterpret_cast<const i32x4 *>(oo + lane * 16);
-                o.io[c] = *reinterpret_cast<const int *>(oo + 1024 + iword * 4);
-                oo += kOpBytes;
-            }
+            o.ao[c] = *reinterpret_cast<const i32x4 *>(oo + c * kOpBytes + lane * 16);
+            o.io[c] = *reinterpret_cast<const int *>(oo + c * kOpBytes + 1024 + iword * 4);
         }
     };
-    // element e (operands in set PA, token rows in ring slot PB, overflow
-    // mask cmask) while element e+1's operands are read into the other set
-    // (its panel byte nbase, overflow mask nmask)
-    auto multiply = [&](auto pa, auto pb, uint32_t cmask, uint32_t nbase, uint32_t nmask) {
+    // element e (operands in set PA, token rows in ring slot PB) while
+    // element e+1's operands are read into the other set (its panel byte
+    // nbase)
+    auto multiply = [&](auto pa, auto pb, uint32_t nbase) {
         constexpr int PA = decltype(pa)::value;
         constexpr int PB = decltype(pb)::value;
         Ops &cur = ops[PA];
@@ -220,15 +217,12 @@ __device__ __forceinline__ void panel_body(const LinearArgs &a, const GeluArg *e
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one matrix instruction
         }
         __builtin_amdgcn_sched_group_barrier(0x008, NT * ST > 2 * NT ? NT * ST - 2 * NT : 0, 0);
-        read_ovf(nxt, nbase, nmask);
+        read_ovf(nxt, nbase);
 #pragma unroll
-        for (int c = 0; c < NT; ++c) {
-            if ((cmask >> c) & 1u) {
+        for (int c = 0; c < NT; ++c)
 #pragma unroll
-                for (int s = 0; s < ST; ++s)
-                    acc[c][s] = __builtin_amdgcn_smfmac_i32_16x16x128_i8(cur.ao[c], bv[PB][s], acc[c][s], cur.io[c], 0, 0);
-            }
-        }
+            for (int s = 0; s < ST; ++s)
+                acc[c][s] = __builtin_amdgcn_smfmac_i32_16x16x128_i8(cur.ao[c], bv[PB][s], acc[c][s], cur.io[c], 0, 0);
     };
 
     // accumulator layout: lane l holds rows 4*(l/16)+r (channels of one
@@ -381,13 +375,9 @@ __device__ __forceinline__ void panel_body(const LinearArgs &a, const GeluArg *e
         return p >= a.n_win ? p - a.n_win : p;
     };
     uint32_t ro[ST], ron[ST];
-    // the window table's entries are wave-uniform: their reads broadcast
-    auto entry = [&](int u, uint32_t &mask, uint32_t &base) {
-        const uint4 e = wtab[phys(u)];
-        mask = __builtin_amdgcn_readfirstlane(e.x);
-        base = __builtin_amdgcn_readfirstlane(e.z) * 16u;
-    };
-    uint32_t cmask = 0, cbase = 0;  // the element being multiplied
+    // panel byte of the element at window u: NT main operands and NT
+    // overflow slots per window
+    auto wbase = [&](int u) { return (uint32_t)phys(u) * (uint32_t)(2 * NT * kOpBytes); };
     // the first R - 1 windows of token rows load while the panel copies are
     // in flight, then the set-up; one barrier after all of them, past which
     // table, panel, scales and GELU table are in LDS
@@ -416,9 +406,8 @@ __device__ __forceinline__ void panel_body(const LinearArgs &a, const GeluArg *e
     wait_vmcnt_le<0>();
     __syncthreads();
     if (n_my > 0) {
-        entry(0, cmask, cbase);
-        read_main(ops[0], cbase);
-        read_ovf(ops[0], cbase, cmask);
+        read_main(ops[0], wbase(0));
+        read_ovf(ops[0], wbase(0));
     }
     static_assert(R % 2 == 0, "ring slots and operand sets alternate together");
     for (int i = 0; i < n_my; ++i) {
@@ -445,11 +434,7 @@ __device__ __forceinline__ void panel_body(const LinearArgs &a, const GeluArg *e
                 if (u < a.n_win) {
                     // the next element: this group's next window, else the
                     // next group's first (a stale read past the last one)
-                    uint32_t nmask, nbase;
-                    entry(u + 1 < a.n_win ? u + 1 : 0, nmask, nbase);
-                    multiply(std::integral_constant<int, U % 2>{}, uc, cmask, nbase, nmask);
-                    cmask = nmask;
-                    cbase = nbase;
+                    multiply(std::integral_constant<int, U % 2>{}, uc, wbase(u + 1 < a.n_win ? u + 1 : 0));
                 }
             });
         }

@@ -117,8 +117,9 @@ constexpr int kMaxOmTables = 8;
 // channel group g and window w, the entry {mask, first, base, 0} at
 // [g][n_win + 1][4] uint32: mask and first as in the overflow table; base =
 // offset, in 16-byte pieces, of the window's operands in the group's panel
-// (the nt main operands, then the window's overflow operands in tile order).
-// Entry n_win holds the panel's total size in its base word.
+// (the nt main operands, then nt overflow operand slots, one per tile, zeros
+// where the tile has none: base = w * 2 * nt * 68). Entry n_win holds the
+// panel's total size in its base word.
 constexpr int kMaxPanTables = 4;
 
 struct DeviceImage {
