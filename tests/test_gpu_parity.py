@@ -168,6 +168,35 @@ def test_same_handle_two_streams(hip):
         assert np.array_equal(y.cpu().numpy(), oracle.acc(x.cpu().numpy(), w))
 
 
+def test_split_reduction_limits(hip, monkeypatch):
+    """The split-reduction kernel covers reductions of up to 32 windows
+    (k <= 4096): at 32 windows it runs with 16 waves of 2 windows; at 33
+    SL_PATH=split falls back to another kernel with the same results. Both
+    with the block layout in and out and the int8 GELU epilogue."""
+    import torch
+    monkeypatch.setenv("SL_PATH", "split")
+    for k, want_split in ((4096, True), (4224, False)):
+        w, sw, b, rng = _case(96, k, 0.2, k)
+        x = rng.integers(-127, 128, (40, k), dtype=np.int8)
+        pw = hip.PackedWeight.pack(w, sw, b)
+        g = oracle.linear(x, w, 0.02, sw, b, oracle.KIND_F32_GELU)
+        so = float(oracle.calibrate_out_scale(g)) or 1.0
+        xd = torch.from_numpy(np.ascontiguousarray(hip.to_t16x32(x, fill=11))).cuda()
+        say(f"split limits k={k}")
+        for kind in (0, 4):
+            y = pw.run(xd, 0.02, kind, out_scale=so, x_layout=1, y_layout=1 if kind == 4 else 0, m_tokens=40)
+            torch.cuda.synchronize()
+            path = hip.last_path()
+            assert path.startswith("split") == want_split, path
+            if want_split:
+                assert "kw=16 wpw=2" in path, path
+            got = y.cpu().numpy()
+            if kind == 4:
+                got = hip.from_t16x32(got, 40, 96)
+            check(kind, got, oracle.linear(x, w, 0.02, sw, b, kind, so=so), f"k={k} kind={kind} {path}")
+        pw.free()
+
+
 @pytest.mark.parametrize("n", [0, 1, 15, 16, 17, 1000, 4096 * 768 + 5])
 def test_quantize_act(hip, n):
     import torch
