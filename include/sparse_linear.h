@@ -228,8 +228,8 @@ int32_t sl_abi_version(void);
  * Thread-local text naming the kernel and workgroup shape of the last
  * successful sparse_linear_run / sparse_linear_run_layout on this thread
  * ("" before the first): "split st,nt kw=K wpw=W" (split reduction, for
- * few tokens), "panel nt,st,nwv,r" (weight-stationary), "direct st,nt,wm,d",
- * "staged st,ct,wm,wn,d" or "resident ...", followed by " gelu=erf" when an
+ * few tokens), "panel nt,st,nwv,r" (weight-stationary), "direct st,nt,wm,d"
+ * or "staged st,ct,wm,wn,d", followed by " gelu=erf" when an
  * int8 GELU epilogue evaluated erf because its output scale (below about
  * 0.015) admits no step table. For tests and tuning; the text is valid until
  * the next run on this thread.
@@ -238,7 +238,7 @@ const char *sl_last_path(void);
 
 /*
  * Kernel selection overrides, for tuning and tests: SL_PATH (split, panel,
- * direct, staged, resident) and the tile shapes SL_TILE / SL_DTILE / SL_PTILE are
+ * direct, staged) and the tile shapes SL_TILE / SL_DTILE / SL_PTILE are
  * read from the environment once, at the first run; sl_reload_env() reads
  * them again (call it after changing them, with no run in flight on any
  * thread).

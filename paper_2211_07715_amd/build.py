@@ -24,8 +24,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 HOST_SOURCES = ["api.cpp", "pack.cpp", "gelu_table.cpp"]
-HIP_SOURCES = ["kernels.hip", "kernels_direct.hip", "kernels_panel.hip", "kernels_resident.hip",
-               "kernels_split.hip"]
+HIP_SOURCES = ["kernels.hip", "kernels_direct.hip", "kernels_panel.hip", "kernels_split.hip"]
 # the benchmark's measurement probes (copy bandwidth, matrix-instruction
 # throughput): a library of their own, not linked into the layer's
 PROBE_SOURCES = ["probe.hip"]

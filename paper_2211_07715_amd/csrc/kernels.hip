@@ -745,22 +745,6 @@ sl_status upload_image(sl_packed_weight *w)
             }
         }
     }
-    // the register-resident kernel's LDS for one workgroup's overflow operands
-    uint32_t res_lds_ovf = 0;
-    if (ti.res_ks) {
-        const int tiles_wg = (kResWaves / ti.res_ks) * kResTiles;
-        for (int32_t t0 = 0; t0 < ti.n_tiles; t0 += tiles_wg) {
-            const int32_t t1 = std::min(t0 + tiles_wg, ti.n_tiles);
-            const uint64_t nb = (uint64_t)(ti.res_dir[(size_t)t1 * ti.res_ks] - ti.res_dir[(size_t)t0 * ti.res_ks]) *
-                                kResOpBytes;
-            res_lds_ovf = (uint32_t)std::max<uint64_t>(res_lds_ovf, std::min<uint64_t>((nb + 1023) / 1024 * 1024,
-                                                                                         UINT32_MAX));
-        }
-    }
-    if ((int64_t)ti.res_ovf.size() > kMaxBufferBytes) {
-        set_error("packed weight image over 2 GiB (n_out x k_in too large for one image)");
-        return SL_ERR_UNSUPPORTED;
-    }
     // the split-reduction kernel's overflow image (the same size as the main
     // image, which is known to fit one buffer)
     std::vector<int8_t> odense(ti.main.size(), 0);
@@ -792,10 +776,6 @@ sl_status upload_image(sl_packed_weight *w)
         o_pan[i] = o_end;
         o_end = align256(o_end + pimgs[i].size());
     }
-    const size_t o_rovf = o_end;
-    o_end = align256(o_end + std::max<size_t>(ti.res_ovf.size(), 16));
-    const size_t o_rdir = o_end;
-    o_end = align256(o_end + std::max<size_t>(ti.res_dir.size() * sizeof(uint32_t), 16));
     const size_t o_ovfd = o_end;
     o_end = align256(o_end + b_main);
     const size_t total = o_end;
@@ -828,13 +808,6 @@ sl_status upload_image(sl_packed_weight *w)
         w->dev.pan[i] = pimgs[i].empty() ? nullptr : reinterpret_cast<const int8_t *>(p + o_pan[i]);
     }
     w->dev.n_pan = (int32_t)pnts.size();
-    if (!ti.res_ovf.empty()) HIP_TRY(hipMemcpy(p + o_rovf, ti.res_ovf.data(), ti.res_ovf.size(), hipMemcpyHostToDevice));
-    if (!ti.res_dir.empty())
-        HIP_TRY(hipMemcpy(p + o_rdir, ti.res_dir.data(), ti.res_dir.size() * sizeof(uint32_t), hipMemcpyHostToDevice));
-    w->dev.rovf = reinterpret_cast<const int8_t *>(p + o_rovf);
-    w->dev.rovf_bytes = (uint32_t)ti.res_ovf.size();
-    w->dev.rdir = reinterpret_cast<const uint32_t *>(p + o_rdir);
-    w->dev.res_lds_ovf = res_lds_ovf;
     if (!odense.empty()) HIP_TRY(hipMemcpy(p + o_ovfd, odense.data(), odense.size(), hipMemcpyHostToDevice));
     w->dev.ovfd = reinterpret_cast<const int8_t *>(p + o_ovfd);
     w->dev.ovfd_bytes = (uint32_t)odense.size();
@@ -1086,56 +1059,6 @@ static sl_status choose_panel_cfg(LinearArgs &a, const sl_packed_weight *w, int3
     return SL_OK;
 }
 
-// The register-resident kernel for one launch chunk (a.x, a.y, a.m set):
-// SL_ERR_UNSUPPORTED when the weight has no resident form (k_in > 3072) or
-// the launch does not fit in LDS.
-static sl_status try_resident(const sl_packed_weight *w, const LinearArgs &la, bool xt, bool yt, int32_t run_kind,
-                              const GeluArg *ep, hipStream_t s)
-{
-    const TileImage &ti = w->tiles;
-    if (!ti.res_ks) return SL_ERR_UNSUPPORTED;
-    ResArgs a;
-    a.x = la.x;
-    a.y = la.y;
-    a.m = la.m;
-    a.n = w->n_out;
-    a.k = w->k_in;
-    a.main = w->dev.main;
-    a.main_bytes = (uint32_t)ti.main.size();
-    a.rovf = w->dev.rovf;
-    a.rovf_bytes = w->dev.rovf_bytes;
-    a.rdir = w->dev.rdir;
-    a.w_scale = w->dev.w_scale;
-    a.bias = w->dev.bias;
-    a.sx = la.sx;
-    a.inv_so = la.inv_so;
-    a.n_tiles = ti.n_tiles;
-    a.n_win = ti.n_win;
-    a.ks = ti.res_ks;
-    a.tiles_wg = (kResWaves / a.ks) * kResTiles;
-    a.n_cg = (a.n_tiles + a.tiles_wg - 1) / a.tiles_wg;
-    a.passes = (int32_t)std::min<int64_t>((a.m + 15) / 16, INT32_MAX);
-    int dev = 0, n_cu = 0;
-    HIP_TRY(hipGetDevice(&dev));
-    HIP_TRY(hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev));
-    a.wg_per_cg = (int32_t)std::max<int64_t>(1, std::min<int64_t>(a.passes, std::max(1, n_cu / a.n_cg)));
-    a.x_cb = la.x_cb;
-    a.y_cb = la.y_cb;
-    a.cbw = 4 * a.n_win;
-    a.xt = xt ? 1 : 0;
-    a.yt = yt ? 1 : 0;
-    a.lds_ovf = w->dev.res_lds_ovf;
-    const int out_bytes = (run_kind == SL_EPI_I8 || run_kind == SL_EPI_I8_GELU || run_kind == kEpiI8GeluErf) ? 1 : 4;
-    const ResLds L = res_lds_layout(a.cbw, a.tiles_wg, a.ks, out_bytes, run_kind == SL_EPI_I8_GELU, a.lds_ovf);
-    if (L.total > kLdsMax) return SL_ERR_UNSUPPORTED;
-    const int64_t grid = (int64_t)a.n_cg * a.wg_per_cg;
-    if (grid > 0x7fffffff) return SL_ERR_UNSUPPORTED;
-    sl_status st_ = launch_resident(a, ep, run_kind, (uint32_t)grid, L.total, s);
-    if (st_ != SL_OK) return st_;
-    set_last_path("resident ks=%d groups=%dx%d lds=%u", a.ks, a.n_cg, a.wg_per_cg, L.total);
-    return SL_OK;
-}
-
 sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int32_t x_layout, int64_t m, float sx,
                         int32_t kind, float inv_so, void *y, int32_t y_layout, void *stream)
 {
@@ -1228,11 +1151,6 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int32_t x_la
             a.ovf = w->dev.ovf;
             a.ovf_bytes = (uint32_t)ti.ovf.size();
             continue;
-        }
-        if (vec && strcmp(path, "resident") == 0) {
-            sl_status rst = try_resident(w, a, xt, yt, run_kind, run_kind == SL_EPI_I8_GELU ? &ga : nullptr, s);
-            if (rst == SL_OK) continue;
-            if (rst != SL_ERR_UNSUPPORTED) return rst;
         }
         const bool force_panel = strcmp(path, "panel") == 0;
         const bool auto_path = !*path;

@@ -194,95 +194,6 @@ static sl_status build_tiles(sl_packed_weight *p)
     return SL_OK;
 }
 
-// The consolidated overflow operands of the register-resident kernel (see
-// TileImage): per (tile, K slice), the groups where some block-row of the
-// tile stores 3 or 4 blocks, ascending, 32 to an operand; a block-row's third
-// and fourth blocks of such a group take the value pair of the group's slot,
-// exactly as they would in a per-window overflow operand.
-static sl_status build_resident(sl_packed_weight *p)
-{
-    TileImage &ti = p->tiles;
-    ti.res_ks = res_k_split(ti.n_win);
-    ti.res_ops = 0;
-    ti.res_ovf.clear();
-    ti.res_dir.clear();
-    if (!ti.res_ks) return SL_OK;
-    const int ks = ti.res_ks;
-    const int32_t nbr = p->n_out / 4, k_in = p->k_in;
-    ti.res_dir.assign((size_t)ti.n_tiles * ks + 1, 0);
-    int gq[32], gt[32];
-    for (int g = 0; g < 32; ++g) group_slot(g, &gq[g], &gt[g]);
-    struct Ent {
-        int32_t grp;
-        int jb;
-        int pos[2];
-        uint32_t blk[2];
-    };
-    std::vector<Ent> ents;
-    std::vector<int32_t> grps;
-    uint32_t n_ops = 0;
-    int8_t op[kResOpBytes];
-    for (int32_t t = 0; t < ti.n_tiles; ++t) {
-        for (int s = 0; s < ks; ++s) {
-            ti.res_dir[(size_t)t * ks + s] = n_ops;
-            const int32_t cbeg = s * kResWin * kWin, cend = std::min(k_in, (s + 1) * kResWin * kWin);
-            ents.clear();
-            for (int jb = 0; jb < 4; ++jb) {
-                const int32_t g = 4 * t + jb;
-                if (g >= nbr) break;
-                const uint16_t *c0 = p->col.data() + p->row_ptr[g], *c1 = p->col.data() + p->row_ptr[g + 1];
-                uint32_t e = (uint32_t)(std::lower_bound(c0, c1, (uint16_t)std::min(cbeg, 65535)) - p->col.data());
-                if (cbeg > 65535) e = p->row_ptr[g + 1];
-                while (e < p->row_ptr[g + 1] && p->col[e] < cend) {
-                    const int32_t grp = p->col[e] / 4;
-                    uint32_t eg[4];
-                    int n = 0;
-                    while (e < p->row_ptr[g + 1] && p->col[e] < cend && p->col[e] / 4 == grp) eg[n++] = e++;
-                    if (n >= 3) {
-                        Ent en;
-                        en.grp = grp;
-                        en.jb = jb;
-                        make_pair(p, eg + 2, n - 2, en.pos, en.blk);
-                        ents.push_back(en);
-                    }
-                }
-            }
-            grps.clear();
-            for (const Ent &en : ents) grps.push_back(en.grp);
-            std::sort(grps.begin(), grps.end());
-            grps.erase(std::unique(grps.begin(), grps.end()), grps.end());
-            for (size_t o = 0; o < grps.size(); o += 32) {
-                memset(op, 0, sizeof(op));
-                uint32_t idx[16];
-                for (int i = 0; i < 16; ++i) idx[i] = kIdleIdx;
-                uint32_t gp[32] = {};
-                const size_t nv = std::min<size_t>(32, grps.size() - o);
-                for (size_t v = 0; v < nv; ++v) gp[v] = res_group_offset(grps[o + v]);
-                for (const Ent &en : ents) {
-                    const size_t v = (size_t)(std::lower_bound(grps.begin(), grps.end(), en.grp) - grps.begin());
-                    if (v < o || v >= o + nv) continue;
-                    const int q = gq[v - o], pt = gt[v - o];
-                    uint32_t &ix = idx[en.jb * 4 + q];
-                    ix &= ~(0xFu << (4 * pt));
-                    ix |= (uint32_t)(en.pos[0] | (en.pos[1] << 2)) << (4 * pt);
-                    for (int sp = 0; sp < 2; ++sp) {
-                        if (en.blk[sp] == UINT32_MAX) continue;
-                        for (int r = 0; r < 4; ++r)
-                            op[(16 * q + 4 * en.jb + r) * 16 + 2 * pt + sp] = p->vals[4 * (size_t)en.blk[sp] + r];
-                    }
-                }
-                memcpy(op + 1024, idx, 64);
-                memcpy(op + kOpBytes, gp, 128);
-                ti.res_ovf.insert(ti.res_ovf.end(), op, op + kResOpBytes);
-                ++n_ops;
-            }
-        }
-    }
-    ti.res_dir[(size_t)ti.n_tiles * ks] = n_ops;
-    ti.res_ops = n_ops;
-    return SL_OK;
-}
-
 sl_status build_host_image(const int8_t *w, int32_t n_out, int32_t k_in, const float *w_scale,
                            const float *bias, sl_packed_weight *p)
 {
@@ -297,8 +208,7 @@ sl_status build_host_image(const int8_t *w, int32_t n_out, int32_t k_in, const f
         sl_status st = build_bsr(w, n_out, k_in, p);
         if (st != SL_OK) return st;
         st = build_tiles(p);
-        if (st != SL_OK) return st;
-        return build_resident(p);
+        return st;
     } catch (const std::bad_alloc &) {
         set_error("host allocation failed while packing");
         return SL_ERR_OOM;
@@ -308,8 +218,7 @@ sl_status build_host_image(const int8_t *w, int32_t n_out, int32_t k_in, const f
 // Inverse of build_tiles: every value of every operand is placed back at the
 // (channel, column) the instruction reads it for. Fails on values beyond the
 // matrix, two values at one position, or a pair whose two positions coincide.
-static sl_status decode_operand(const int8_t *op, int32_t t, int32_t w, const sl_packed_weight *p, int8_t *dense,
-                                const uint32_t *gp = nullptr)
+static sl_status decode_operand(const int8_t *op, int32_t t, int32_t w, const sl_packed_weight *p, int8_t *dense)
 {
     const int32_t k_in = p->k_in;
     for (int lane = 0; lane < 64; ++lane) {
@@ -326,11 +235,7 @@ static sl_status decode_operand(const int8_t *op, int32_t t, int32_t w, const sl
                     return SL_ERR_INVALID_ARG;
                 }
                 const int32_t n = t * kTileN + i;
-                const int vg = entry_group(q, pt);
-                // a consolidated operand's slot names its group by its offset
-                // in the token tile: (g / 8) * 512 + 4 * (g % 8)
-                const int32_t grp = gp ? (int32_t)(gp[vg] / 512u) * 8 + (int32_t)(gp[vg] % 512u) / 4
-                                       : w * (kWin / 4) + vg;
+                const int32_t grp = w * (kWin / 4) + entry_group(q, pt);
                 const int32_t col = 4 * grp + (sp ? pos1 : pos0);
                 if (n >= p->n_out || col >= k_in) {
                     set_error("tile image holds a value outside the matrix");
@@ -366,40 +271,6 @@ sl_status decode_tile_image(const sl_packed_weight *p, int8_t *dense)
                 st = decode_operand(&ti.ovf[(size_t)o * kOpBytes], t, w, p, dense);
                 if (st != SL_OK) return st;
             }
-        }
-    }
-    // The register-resident form (main operands plus consolidated overflow
-    // operands) must decode to the same weight.
-    if (ti.res_ks) {
-        std::vector<int8_t> alt((size_t)p->n_out * p->k_in, 0);
-        for (int32_t w = 0; w < ti.n_win; ++w)
-            for (int32_t t = 0; t < ti.n_tiles; ++t) {
-                sl_status st = decode_operand(&ti.main[((size_t)w * ti.n_tiles + t) * kOpBytes], t, w, p, alt.data());
-                if (st != SL_OK) return st;
-            }
-        for (int32_t t = 0; t < ti.n_tiles; ++t)
-            for (int s = 0; s < ti.res_ks; ++s) {
-                const int32_t cbeg = s * kResWin * kWin, cend = std::min(p->k_in, (s + 1) * kResWin * kWin);
-                for (uint32_t o = ti.res_dir[(size_t)t * ti.res_ks + s]; o < ti.res_dir[(size_t)t * ti.res_ks + s + 1];
-                     ++o) {
-                    const int8_t *op = &ti.res_ovf[(size_t)o * kResOpBytes];
-                    uint32_t gp[32];
-                    memcpy(gp, op + kOpBytes, 128);
-                    // (unused slots hold offset 0 and no value)
-                    for (int v = 0; v < 32; ++v) {
-                        const int32_t c = 4 * ((int32_t)(gp[v] / 512u) * 8 + (int32_t)(gp[v] % 512u) / 4);
-                        if (gp[v] % 4 || (gp[v] != 0 && (c < cbeg || c >= cend))) {
-                            set_error("consolidated overflow operand names a group outside its K slice");
-                            return SL_ERR_INVALID_ARG;
-                        }
-                    }
-                    sl_status st = decode_operand(op, t, 0, p, alt.data(), gp);
-                    if (st != SL_OK) return st;
-                }
-            }
-        if (memcmp(alt.data(), dense, alt.size()) != 0) {
-            set_error("the register-resident image decodes to a different weight");
-            return SL_ERR_INVALID_ARG;
         }
     }
     return SL_OK;

@@ -364,77 +364,4 @@ sl_status panel_resident(PanelCfg c, size_t lds, int *out);
 // kMaxDevices entries per kernel instance.
 sl_status persistent_grid(const void *fn, int threads, size_t lds, int *cache, int *out);
 
-// ---------------------------------------------------------------------------
-// Register-resident kernel (kernels_resident.hip): 4 compute waves, one per
-// SIMD, and one memory wave; compute wave w owns channel part w / ks
-// (kResTiles tiles) and K slice w % ks (kResWin windows) of its workgroup's
-// channel group, whose main operands it holds in registers; token passes of
-// 16 tokens stream through LDS.
-constexpr int kResWaves = 4;                   // compute waves
-constexpr int kResThreads = 64 * (kResWaves + 1);
-
-struct ResArgs {
-    const int8_t *x;
-    void *y;
-    int64_t m;             // tokens of this launch
-    int32_t n, k;
-    const int8_t *main;    // main operands [n_win][n_tiles][kOpBytes]
-    uint32_t main_bytes;
-    const int8_t *rovf;    // consolidated overflow operands [res_ops][kResOpBytes]
-    uint32_t rovf_bytes;
-    const uint32_t *rdir;  // [n_tiles * ks + 1]
-    const float *w_scale;
-    const float *bias;
-    float sx;
-    float inv_so;
-    int32_t n_tiles, n_win;
-    int32_t ks;            // compute waves a reduction is split over: 1, 2 or 4
-    int32_t tiles_wg;      // channel tiles per workgroup: (kResWaves / ks) * kResTiles
-    int32_t n_cg;          // channel groups
-    int32_t wg_per_cg;     // workgroups (token slices) per channel group
-    int32_t passes;        // token passes of this launch (16 tokens each)
-    int32_t x_cb;          // 32-feature column blocks of x (block layout)
-    int32_t y_cb;          // 32-channel column blocks of y (block layout)
-    int32_t cbw;           // 32-column blocks of the LDS token tile: 4 n_win
-    int32_t xt, yt;        // x / y in SL_LAYOUT_T16X32
-    uint32_t lds_ovf;      // LDS bytes for the overflow operands (a multiple of 1024)
-};
-
-// LDS layout of a launch (byte offsets, all multiples of 16): two token-tile
-// buffers (16 tokens x all columns each); two output staging buffers (16 token
-// rows of the group's channels, out_bytes each, rows ostride bytes apart); the
-// group's scales and biases; the GELU table; the index words of the group's
-// main operands ([tile][window][16 words]); an all-zero overflow operand
-// (stands in for an absent one); the partial sums of a split reduction (in
-// the pass's own token-tile buffer when it is large enough: every wave has
-// finished reading it by then); the consolidated overflow operands.
-struct ResLds {
-    uint32_t xbuf, out, ostride, obuf, vec, tab, idx, dummy, red, ovf, total;
-};
-constexpr uint32_t kResRedBytes = (uint32_t)kResWaves * kResTiles * 1024u;
-__host__ __device__ inline ResLds res_lds_layout(int cbw, int tiles_wg, int ks, int out_bytes, bool gelu,
-                                                 uint32_t ovf_bytes)
-{
-    ResLds l;
-    l.xbuf = (uint32_t)cbw * 512u;
-    l.out = 2 * l.xbuf;
-    l.ostride = (uint32_t)tiles_wg * kTileN * (uint32_t)out_bytes + 16u;
-    l.obuf = 16u * l.ostride;
-    l.vec = l.out + 2 * l.obuf;
-    l.tab = l.vec + (uint32_t)tiles_wg * kTileN * 8u;
-    l.idx = l.tab + (gelu ? (uint32_t)kGeluLds : 0u);
-    l.dummy = l.idx + (uint32_t)tiles_wg * (uint32_t)(cbw / 4) * 64u;
-    uint32_t end = l.dummy + (uint32_t)kResOpBytes;
-    l.red = 0xffffffffu;  // in the pass's token-tile buffer
-    if (ks > 1 && l.xbuf < kResRedBytes) {
-        l.red = end;
-        end += kResRedBytes;
-    }
-    l.ovf = end;
-    l.total = l.ovf + ovf_bytes;
-    return l;
-}
-sl_status launch_resident(const ResArgs &a, const GeluArg *ep, int32_t run_kind, uint32_t grid, size_t lds,
-                          hipStream_t stream);
-
 }  // namespace sl

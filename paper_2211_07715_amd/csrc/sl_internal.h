@@ -48,36 +48,8 @@ struct TileImage {
     std::vector<int8_t> main;
     std::vector<int8_t> ovf;
     std::vector<uint32_t> ovf_ptr;
-    // Register-resident kernel (kernels_resident.hip): each wave holds the
-    // main operands of kResTiles tiles x kResWin windows in registers; the
-    // reduction is split over res_ks waves (1, 2 or 4; 0: k_in too long for
-    // this form). The third and fourth stored blocks of a (block-row, aligned
-    // 4-column group) do not go to a per-window overflow operand but to one of
-    // the tile's consolidated overflow operands for its K slice (the res_ks
-    // slices of kResWin windows each): each holds up to 32 such groups from
-    // anywhere in the slice, in "virtual group" slots, with a table giving
-    // each slot's group as a byte offset in the kernel's LDS token tile; the
-    // kernel gathers those 4-byte column groups into the dense operand.
-    //   res_ovf  [res_ops][kResOpBytes]: values and index words as a main
-    //            operand (virtual group v in place of window group v), then
-    //            32 uint32 offsets (group g at (g / 8) * 512 + 4 * (g % 8))
-    //   res_dir  [n_tiles * res_ks + 1]: operands of (tile t, slice s) are
-    //            res_dir[t * res_ks + s] .. res_dir[t * res_ks + s + 1] - 1
-    int32_t res_ks = 0;
-    int64_t res_ops = 0;
-    std::vector<int8_t> res_ovf;
-    std::vector<uint32_t> res_dir;
 };
 
-constexpr int kResTiles = 5;  // channel tiles per wave
-constexpr int kResWin = 6;    // 128-column windows per wave
-constexpr int kResOpBytes = kOpBytes + 128;  // 1216 = 76 pieces of 16 bytes
-constexpr int kResMaxKs = 4;
-// waves the reduction of n_win windows is split over, 0 if too long
-inline int res_k_split(int n_win) { return n_win <= kResWin ? 1 : n_win <= 2 * kResWin ? 2 : n_win <= 4 * kResWin ? 4 : 0; }
-// byte offset of aligned column group g (4 columns) in the kernel's LDS token
-// tile of 32-column blocks of 512 bytes (16 tokens x 32 bytes)
-inline uint32_t res_group_offset(int g) { return (uint32_t)(g / 8) * 512u + 4u * (uint32_t)(g % 8); }
 
 // Step table of the fused GELU(erf) + int8 requantisation (gelu_table.cpp).
 constexpr int kGeluCells = 448;
@@ -143,17 +115,10 @@ struct DeviceImage {
     // 0: the panels do not fit in LDS and there is no such image)
     uint32_t pan_stride[kMaxPanTables] = {};
     const int8_t *pan[kMaxPanTables] = {};
-    // register-resident kernel: consolidated overflow operands and their
-    // directory (TileImage::res_ovf / res_dir); res_lds_ovf = the most LDS
-    // one workgroup's operands take, rounded up to whole 1024-byte copies
-    const int8_t *rovf = nullptr;
-    uint32_t rovf_bytes = 0;
     // split-reduction kernel: the overflow operands in the main image's
     // order, one slot per (window, tile), zeros where the tile has none
     const int8_t *ovfd = nullptr;
     uint32_t ovfd_bytes = 0;
-    const uint32_t *rdir = nullptr;
-    uint32_t res_lds_ovf = 0;
     int64_t bytes = 0;
 };
 
@@ -189,7 +154,7 @@ void clear_error();
 // Kernel-choice overrides for tests and tuning (SL_PATH, SL_TILE, SL_DTILE,
 // SL_PTILE), read from the environment once and again on sl_reload_env()
 struct EnvCfg {
-    char path[16];  // "" (automatic), "panel", "direct", "staged", "resident", "split"
+    char path[16];  // "" (automatic), "split", "panel", "direct", "staged"
     int tile[5];    // SL_TILE "st,ct,wm,wn,d"; tile[0] == 0: unset
     int dtile[4];   // SL_DTILE "st,nt,wm,d"
     int ptile[4];   // SL_PTILE "nt,st,nwv,r"
