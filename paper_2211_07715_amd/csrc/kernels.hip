@@ -648,12 +648,10 @@ sl_status upload_image(sl_packed_weight *w)
         set_error("packed weight image over 2 GiB (n_out x k_in too large for one image)");
         return SL_ERR_UNSUPPORTED;
     }
-    // overflow tables, one per tile-group size of the shape table
+    // overflow tables, one per tile-group size of the staged kernel's shapes
     std::vector<int> nts;
     for (const TileCfg &c : kCfgs)
         if (std::find(nts.begin(), nts.end(), c.nt()) == nts.end()) nts.push_back(c.nt());
-    for (const DirectCfg &c : kDirectCfgs)
-        if (std::find(nts.begin(), nts.end(), c.nt) == nts.end()) nts.push_back(c.nt);
     if ((int)nts.size() > kMaxOmTables) {
         set_error("internal: too many tile-group sizes");
         return SL_ERR_UNSUPPORTED;
@@ -745,8 +743,10 @@ sl_status upload_image(sl_packed_weight *w)
             }
         }
     }
-    // the split-reduction kernel's overflow image (the same size as the main
-    // image, which is known to fit one buffer)
+    // the dense overflow image of the split-reduction and direct kernels: a
+    // tile's overflow operand of a window at the offset of its main operand,
+    // zeros where it has none (the same size as the main image, which is
+    // known to fit one buffer)
     std::vector<int8_t> odense(ti.main.size(), 0);
     {
         const size_t pstride = (size_t)ti.n_tiles + 1;
@@ -1187,7 +1187,7 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int32_t x_la
         a.om = nullptr;
         for (int i = 0; i < w->dev.n_om; ++i)
             if (w->dev.om_nt[i] == nt) a.om = w->dev.om[i];
-        if (!a.om) {
+        if (!direct && !a.om) {
             set_error("internal: no overflow table for the chosen workgroup shape");
             return SL_ERR_UNSUPPORTED;
         }
@@ -1199,7 +1199,11 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int32_t x_la
         }
         sl_status st;
         if (direct) {
+            a.ovf = w->dev.ovfd;  // (restored below for the other kernels' chunks)
+            a.ovf_bytes = w->dev.ovfd_bytes;
             st = launch_direct(a, run_kind == SL_EPI_I8_GELU ? &ga : nullptr, run_kind, dcfg, xt, yt, s);
+            a.ovf = w->dev.ovf;
+            a.ovf_bytes = (uint32_t)ti.ovf.size();
             set_last_path("direct %d,%d,%d,%d", dcfg.st, dcfg.nt, dcfg.wm, dcfg.d);
         } else {
             set_last_path("staged %d,%d,%d,%d,%d", cfg.st, cfg.ct, cfg.wm, cfg.wn, cfg.d);

@@ -14,12 +14,13 @@
 // traffic of a window and leaves LDS bandwidth to the weight operands.
 //
 // Copy waves stream each window's weight operands into a ring of D LDS
-// buffers: the NT main operands, the overflow mask of the item's tiles, and
-// the overflow operands present in the window, packed (rank order of their
-// tiles) so that only present operands are copied. A copy instruction of the
-// packed region that would hold none is replaced by a one-lane copy, which
-// keeps the number of copies per window fixed for the waits that count them.
-// Work items (token tile x channel group) are spread over a persistent grid.
+// buffers: the NT main operands and the NT overflow operand slots, both read
+// at the same offsets from the main image and from the dense overflow image
+// (zeros where a tile has no overflow operand). No table lies on the way to
+// a copy's address, so the first element's copies start at kernel entry, and
+// every window takes the same number of copies, which keeps the waits that
+// count them constant. Work items (token tile x channel group) are spread
+// over a persistent grid.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -102,12 +103,6 @@ __device__ __forceinline__ void direct_body(const LinearArgs &a, const GeluArg *
     static_assert((D - 1) * S::COPIES < 64, "outstanding copies must fit the 6-bit vector-memory counter");
 
     if (copier) {
-        typedef const __attribute__((address_space(4))) uint64_t *const_u64_ptr;
-        const const_u64_ptr omt = (const_u64_ptr)(a.om);
-        auto om_at = [&](const ItemIter &it, int pwin) {
-            const uint64_t v = omt[(size_t)pwin * a.n_cgroups + it.cg];
-            return make_uint2((uint32_t)v, (uint32_t)(v >> 32));
-        };
         const __amdgpu_buffer_rsrc_t mr =
             __builtin_amdgcn_make_buffer_rsrc((void *)a.main, 0, (int)a.main_bytes, kRsrcWord3);
         const __amdgpu_buffer_rsrc_t orc =
@@ -147,80 +142,47 @@ __device__ __forceinline__ void direct_body(const LinearArgs &a, const GeluArg *
         item_offsets();
 
         // Copy k (0 <= k < COPIES) of the cursor's element (physical window
-        // w) into ring buffer bi: main operands, then the overflow operands
-        // into the slot of their tile (o: the element's overflow entry: mask
-        // of the item's tiles that have one, index of the first; zeros for
-        // the others).
-        auto copy = [&](int k, int w, int bi, uint2 o) {
+        // w) into ring buffer bi: main operands, then overflow slots.
+        auto copy = [&](int k, int w, int bi) {
             int8_t *b = smem + bi * S::BUF;
-            if (k < S::CA) {
+            const uint32_t wo = (uint32_t)w * wstride;
+            if (k < S::CA)
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(mr, (lds_void *)(b + (k * S::NW + pw) * 1024), 16, aoff[k],
-                                                         (uint32_t)w * wstride, 0, 0);
-            } else {
-                const int i = k - S::CA;
-                const uint32_t t = (uint32_t)atile[i];
-                const bool has = t < 32u && ((o.x >> t) & 1u);
-                const uint32_t rank = __builtin_popcount(o.x & ((1u << (t & 31u)) - 1u));
-                const uint32_t off = has ? (o.y + rank) * (uint32_t)kOpBytes + (uint32_t)apiece16[i] : kOob;
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(orc, (lds_void *)(b + S::AB + (i * S::NW + pw) * 1024), 16,
-                                                         off, 0, 0, 0);
-            }
+                                                         wo, 0, 0);
+            else
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(orc, (lds_void *)(b + S::AB + ((k - S::CA) * S::NW + pw) * 1024),
+                                                         16, aoff[k - S::CA], wo, 0, 0);
         };
 
-        // Prologue: the overflow entries of elements 0..D-1 start loading; the
-        // main operands of those elements are copied; a bare barrier (A)
-        // publishes the epilogue table the compute waves filled; the overflow
-        // operands follow; once element 0 has landed a second barrier (B)
-        // publishes it.
-        uint2 o[D];
-        {
-            const ItemIter ic0 = ic;
-            const int kc0 = kc, wc0 = wc;
-#pragma unroll
-            for (int d = 0; d < D; ++d) {
-                o[d] = om_at(ic, cur_w());
-                if (++wc == a.n_win) {
-                    wc = 0;
-                    if (++kc < n_my) ic.next();
-                }
-            }
-            ic = ic0;
-            kc = kc0;
-            wc = wc0;
-        }
-        int wp[D];
+        // Prologue: the copies of elements 0..D-1, element by element; a bare
+        // barrier (A) publishes the epilogue table the compute waves filled;
+        // once element 0 has landed a second barrier (B) publishes it.
 #pragma unroll
         for (int d = 0; d < D; ++d) {
-            wp[d] = cur_w();
+            const int w = cur_w();
 #pragma unroll
-            for (int k = 0; k < S::CA; ++k) copy(k, wp[d], d, make_uint2(0u, 0u));
+            for (int k = 0; k < S::COPIES; ++k) copy(k, w, d);
             advance();
         }
         __builtin_amdgcn_s_barrier();  // (A)
         asm volatile("" ::: "memory");
-#pragma unroll
-        for (int d = 0; d < D; ++d) {
-#pragma unroll
-            for (int k = S::CA; k < S::COPIES; ++k) copy(k, wp[d], d, o[d]);
-        }
-        uint2 onx = om_at(ic, cur_w());  // entry of element D
-        wait_vmcnt_le<(D - 1) * S::CA>();  // element 0 landed
-        __builtin_amdgcn_s_barrier();      // (B)
+        wait_vmcnt_le<(D - 1) * S::COPIES>();  // element 0 landed
+        __builtin_amdgcn_s_barrier();          // (B)
         asm volatile("" ::: "memory");
 
-        // step e: copies of element e+D into the buffer of element e; the
-        // overflow entry of the next element loads across the next barrier
+        // step e: wait until element e+1 has landed (the copies issued after
+        // it are those of the D-2 elements that follow it), then copy element
+        // e+D into the buffer of element e
         auto cstep = [&](int64_t e, int u) {
-            if (e + 1 < steps) wait_window_landed<D, S::CA, S::COPIES>((int)(e < D ? e : D));
+            if (e + 1 < steps) wait_vmcnt_le<(D - 2) * S::COPIES>();
             // a bare barrier: __syncthreads() would also wait for the later
             // elements' copies still in flight
             __builtin_amdgcn_s_barrier();
             asm volatile("" ::: "memory");
             const int w = cur_w();
 #pragma unroll
-            for (int k = 0; k < S::COPIES; ++k) copy(k, w, u, onx);
+            for (int k = 0; k < S::COPIES; ++k) copy(k, w, u);
             advance();
-            onx = om_at(ic, cur_w());
         };
         int64_t e = 0;
         for (; e + D <= steps; e += D) {

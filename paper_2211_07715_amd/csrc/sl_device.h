@@ -59,7 +59,8 @@ struct LinearArgs {
     int32_t n;
     int32_t k;
     const int8_t *main;
-    const int8_t *ovf;
+    const int8_t *ovf;    // compact overflow operands (staged, weight-stationary kernels) or the dense
+                          // overflow image (split-reduction, direct kernels)
     uint32_t main_bytes;  // image sizes: the range of the buffer loads
     uint32_t ovf_bytes;
     const uint32_t *om;  // overflow table of this launch's tile-group size, [n_win][n_cgroups][2]
