@@ -986,8 +986,9 @@ constexpr int32_t kPanelMaxWin = 8;
 // Weight-stationary shape for a launch of a.m tokens: the compiled shapes
 // whose largest panel fits in LDS are scored by the bytes their workgroups
 // read (token rows once per channel group, the panel once per workgroup)
-// spread over the CUs they keep busy; SL_PTILE="nt,st,nwv,r" overrides. Fills a's channel-group and slice
-// fields; SL_ERR_UNSUPPORTED when no panel fits.
+// spread over the CUs they keep busy, with a small preference for more
+// resident waves a SIMD; SL_PTILE="nt,st,nwv,r" overrides. Fills a's
+// channel-group and slice fields; SL_ERR_UNSUPPORTED when no panel fits.
 static sl_status choose_panel_cfg(LinearArgs &a, const sl_packed_weight *w, int32_t run_kind, bool yt, PanelCfg *out,
                                   size_t *lds_out)
 {
@@ -1030,29 +1031,36 @@ static sl_status choose_panel_cfg(LinearArgs &a, const sl_packed_weight *w, int3
         if (res < 1) continue;
         const int64_t n_cg = (w->tiles.n_tiles + c.nt - 1) / c.nt;
         const int64_t groups = (mpad + c.tg() - 1) / c.tg();
-        // slices: enough workgroups to fill the resident slots once
-        const int64_t want = std::max<int64_t>(1, res / n_cg);
-        const int64_t sg = std::max<int64_t>(1, (groups + want - 1) / want);
-        const int64_t n_sl = (groups + sg - 1) / sg;
-        const int64_t nwg = n_cg * n_sl;
-        if (nwg > 0x7fffffff) continue;
-        // busy CUs and the bytes each reads
-        const double cus = (double)std::min<int64_t>(n_cu, nwg);
-        const double bytes = (double)a.m * w->k_in * n_cg + (double)nwg * pieces * 16.0;
-        // waves per workgroup without a token group idle
-        const double wave_use = std::min(1.0, (double)sg / c.nwv);
-        const double cost = bytes / cus / wave_use;
-        if (!found || cost < best_cost) {
-            found = true;
-            best_cost = cost;
-            *out = c;
-            *lds_out = lds;
-            a.n_cgroups = (int32_t)n_cg;
-            a.n_slices = (int32_t)n_sl;
-            a.slice_groups = (int32_t)sg;
-            a.pan = w->dev.pan[pi];
-            a.pan_bytes = (uint32_t)(n_cg * w->dev.pan_stride[pi]);
-            a.pan_instr = (int32_t)(w->dev.pan_stride[pi] / 1024);
+        // slices: enough workgroups to fill the resident slots once, or one
+        // workgroup a CU (fewer panel fills, more token groups a wave),
+        // whichever scores better
+        for (int64_t want : {res / n_cg, (int64_t)n_cu / n_cg}) {
+            want = std::max<int64_t>(1, want);
+            const int64_t sg = std::max<int64_t>(1, (groups + want - 1) / want);
+            const int64_t n_sl = (groups + sg - 1) / sg;
+            const int64_t nwg = n_cg * n_sl;
+            if (nwg > 0x7fffffff) continue;
+            // busy CUs and the bytes each reads
+            const double cus = (double)std::min<int64_t>(n_cu, nwg);
+            const double bytes = (double)a.m * w->k_in * n_cg + (double)nwg * pieces * 16.0;
+            // waves per workgroup without a token group idle; among shapes
+            // that read the same bytes, more resident waves a SIMD hide more
+            // latency
+            const double wave_use = std::min(1.0, (double)sg / c.nwv);
+            const double simd_waves = std::min(4.0, (double)std::min<int64_t>(res, nwg) / n_cu * c.nwv / 4.0);
+            const double cost = bytes / cus / wave_use / (1.0 + 0.1 * simd_waves);
+            if (!found || cost < best_cost) {
+                found = true;
+                best_cost = cost;
+                *out = c;
+                *lds_out = lds;
+                a.n_cgroups = (int32_t)n_cg;
+                a.n_slices = (int32_t)n_sl;
+                a.slice_groups = (int32_t)sg;
+                a.pan = w->dev.pan[pi];
+                a.pan_bytes = (uint32_t)(n_cg * w->dev.pan_stride[pi]);
+                a.pan_instr = (int32_t)(w->dev.pan_stride[pi] / 1024);
+            }
         }
     }
     if (!found) return SL_ERR_UNSUPPORTED;

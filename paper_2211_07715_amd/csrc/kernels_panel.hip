@@ -14,13 +14,14 @@
 // way by the packer -- into LDS once, with no dependent read before the
 // copies, then its waves work through the slice's token groups on their own:
 // a wave loads its token rows (the B operands) straight into registers,
-// R - 1 windows ahead, reads the weight operands from the resident panel at
-// offsets that follow from the window alone, and multiplies every slot, so
-// that no per-tile branch or table read sits in the loop (an absent overflow
-// operand is zeros: its products are zero). Past the one barrier that follows
-// the panel copy and the set-up there is none, so one wave's epilogue
-// overlaps the matrix instructions of the others, and the weight image is read from memory once per workgroup rather
-// than once per token tile.
+// R - 1 windows ahead, reads the weight operands from the resident panel a
+// few tiles ahead of its matrix instructions, at offsets that follow from
+// the window alone, and multiplies every slot, so that no per-tile branch or
+// table read sits in the loop (an absent overflow operand is zeros: its
+// products are zero). Past the one barrier that follows the panel copy and
+// the set-up there is none, so one wave's epilogue overlaps the matrix
+// instructions of the others, and the weight image is read from memory once
+// per workgroup rather than once per token tile.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -168,61 +169,61 @@ __device__ __forceinline__ void panel_body(const LinearArgs &a, const GeluArg *e
     i32x8 bv[R][ST];
     static_assert(R >= 2, "at least one window loads while another is multiplied");
 
-    // Weight operands of one element in registers: the NT main operands and
-    // the NT overflow operand slots with their index words. Two sets
-    // alternate: element e+1's operands are read from the panel while
-    // element e's matrix instructions run.
-    struct Ops {
-        i32x4 av[NT], ao[NT];
-        int ix[NT], io[NT];
+    // Weight operands in registers, a ring of RS tiles (main operand,
+    // overflow slot and their index words) filled LA tiles ahead of the
+    // matrix instructions: while tile c of window u is multiplied, tile
+    // c + LA of the wave's tile stream is read (of window u, else of window
+    // u + 1; past the group's last window that is the first window of the
+    // next group, which uses the same panel). A tile's slot is its place in
+    // the stream modulo RS; RS divides 2 NT and windows are walked in pairs,
+    // so the slot follows from c and the window's parity. Three tiles in
+    // flight (NT = 6) instead of two whole windows leave about 90 registers
+    // for more waves a SIMD; small tile groups keep a whole window ahead, so
+    // that the reads have as many matrix instructions to hide behind.
+    constexpr int RS = NT % 3 == 0 ? 3 : (NT <= 2 ? 2 * NT : NT);
+    constexpr int LA = RS - 1 < NT ? RS - 1 : NT;
+    static_assert((2 * NT) % RS == 0 && LA >= 1, "ring slots follow from the tile and the window's parity");
+    struct TOp {
+        i32x4 av, ao;
+        int ix, io;
     };
-    Ops ops[2];
-    // main operands of the element at panel byte base
-    auto read_main = [&](Ops &o, uint32_t base) {
-        const int8_t *const wb = panel + base;
-#pragma unroll
-        for (int c = 0; c < NT; ++c) {
-            o.av[c] = *reinterpret_cast<const i32x4 *>(wb + c * kOpBytes + lane * 16);
-            o.ix[c] = *reinterpret_cast<const int *>(wb + c * kOpBytes + 1024 + iword * 4);
-        }
+    TOp ring[RS];
+    auto read_tile = [&](TOp &t, uint32_t base, int c) {
+        const int8_t *const wb = panel + base + c * kOpBytes;
+        t.av = *reinterpret_cast<const i32x4 *>(wb + lane * 16);
+        t.ix = *reinterpret_cast<const int *>(wb + 1024 + iword * 4);
+        const int8_t *const oo = panel + base + (NT + c) * kOpBytes;
+        t.ao = *reinterpret_cast<const i32x4 *>(oo + lane * 16);
+        t.io = *reinterpret_cast<const int *>(oo + 1024 + iword * 4);
     };
-    // overflow operand slots of the element
-    auto read_ovf = [&](Ops &o, uint32_t base) {
-        const int8_t *const oo = panel + base + NT * kOpBytes;
-#pragma unroll
-        for (int c = 0; c < NT; ++c) {
-            o.ao[c] = *reinterpret_cast<const i32x4 *>(oo + c * kOpBytes + lane * 16);
-            o.io[c] = *reinterpret_cast<const int *>(oo + c * kOpBytes + 1024 + iword * 4);
-        }
-    };
-    // element e (operands in set PA, token rows in ring slot PB) while
-    // element e+1's operands are read into the other set (its panel byte
-    // nbase)
-    auto multiply = [&](auto pa, auto pb, uint32_t nbase) {
-        constexpr int PA = decltype(pa)::value;
+    // window u (parity PAR; token rows in ring slot PB, panel bytes cbase;
+    // the next window's at nbase)
+    auto multiply = [&](auto par, auto pb, uint32_t cbase, uint32_t nbase) {
+        constexpr int PAR = decltype(par)::value;
         constexpr int PB = decltype(pb)::value;
-        Ops &cur = ops[PA];
-        Ops &nxt = ops[PA ^ 1];
-        read_main(nxt, nbase);
-#pragma unroll
-        for (int c = 0; c < NT; ++c)
-#pragma unroll
-            for (int s = 0; s < ST; ++s)
-                acc[c][s] = __builtin_amdgcn_smfmac_i32_16x16x128_i8(cur.av[c], bv[PB][s], acc[c][s], cur.ix[c], 0, 0);
-        // one operand read before each matrix instruction, so that a read
-        // waiting for room in the LDS queue does not leave the matrix core idle
-#pragma unroll
-        for (int v = 0; v < 2 * NT; ++v) {
-            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one matrix instruction
-        }
-        __builtin_amdgcn_sched_group_barrier(0x008, NT * ST > 2 * NT ? NT * ST - 2 * NT : 0, 0);
-        read_ovf(nxt, nbase);
-#pragma unroll
-        for (int c = 0; c < NT; ++c)
+        static_for<NT>([&](auto cc) {
+            constexpr int C = decltype(cc)::value;
+            constexpr int J = C + LA;
+            if constexpr (J < NT)
+                read_tile(ring[(PAR * NT + J) % RS], cbase, J);
+            else
+                read_tile(ring[(PAR * NT + J) % RS], nbase, J - NT);
+            TOp &t = ring[(PAR * NT + C) % RS];
 #pragma unroll
             for (int s = 0; s < ST; ++s)
-                acc[c][s] = __builtin_amdgcn_smfmac_i32_16x16x128_i8(cur.ao[c], bv[PB][s], acc[c][s], cur.io[c], 0, 0);
+                acc[C][s] = __builtin_amdgcn_smfmac_i32_16x16x128_i8(t.av, bv[PB][s], acc[C][s], t.ix, 0, 0);
+#pragma unroll
+            for (int s = 0; s < ST; ++s)
+                acc[C][s] = __builtin_amdgcn_smfmac_i32_16x16x128_i8(t.ao, bv[PB][s], acc[C][s], t.io, 0, 0);
+            // the four operand reads spread over the tile's matrix
+            // instructions, so that a read waiting for room in the LDS queue
+            // does not leave the matrix core idle
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);       // one LDS read
+                __builtin_amdgcn_sched_group_barrier(0x008, ST / 2, 0);  // matrix instructions
+            }
+        });
     };
 
     // accumulator layout: lane l holds rows 4*(l/16)+r (channels of one
@@ -406,8 +407,8 @@ __device__ __forceinline__ void panel_body(const LinearArgs &a, const GeluArg *e
     wait_vmcnt_le<0>();
     __syncthreads();
     if (n_my > 0) {
-        read_main(ops[0], wbase(0));
-        read_ovf(ops[0], wbase(0));
+#pragma unroll
+        for (int j = 0; j < LA; ++j) read_tile(ring[j], wbase(0), j);
     }
     static_assert(R % 2 == 0, "ring slots and operand sets alternate together");
     for (int i = 0; i < n_my; ++i) {
@@ -432,14 +433,23 @@ __device__ __forceinline__ void panel_body(const LinearArgs &a, const GeluArg *e
                 for (int s = 0; s < ST; ++s) rs[s] = in_cur ? ro[s] : ron[s];
                 load_rows(bv[PS], rs, in_cur ? phys(pu) : (in_next ? phys(pn) : 0), in_cur || in_next);
                 if (u < a.n_win) {
-                    // the next element: this group's next window, else the
-                    // next group's first (a stale read past the last one)
-                    multiply(std::integral_constant<int, U % 2>{}, uc, wbase(u + 1 < a.n_win ? u + 1 : 0));
+                    // the ring reads ahead into this group's next window,
+                    // else the next group's first (a stale read past the
+                    // last group)
+                    multiply(std::integral_constant<int, U % 2>{}, uc, wbase(u), wbase(u + 1 < a.n_win ? u + 1 : 0));
                 }
             });
         }
-        // an odd window count leaves the next element's operands in set 1
-        if (a.n_win & 1) ops[0] = ops[1];
+        // after an odd number of windows the next group's first tiles sit
+        // NT slots on; move them to where its first window reads them
+        if constexpr (NT % RS != 0) {
+            if (a.n_win & 1) {
+                static_for<LA>([&](auto tc) {
+                    constexpr int T = decltype(tc)::value;
+                    ring[T % RS] = ring[(NT + T) % RS];
+                });
+            }
+        }
         epilogue(t0);
         if (has_next) {
 #pragma unroll
@@ -498,6 +508,7 @@ static sl_status launch_panel_cfg(const LinearArgs &a, const GeluArg *ep, size_t
 
 // The compiled shapes: F(NT, ST, NWV, R).
 #define SL_PANEL_SHAPES(F) \
+    F(6, 2, 12, 2)         \
     F(6, 2, 8, 2)          \
     F(4, 2, 8, 2)          \
     F(2, 2, 8, 4)          \

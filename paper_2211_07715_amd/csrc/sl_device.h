@@ -348,7 +348,7 @@ struct PanelCfg {
     int nt, st, nwv, r;
     int tg() const { return 16 * st; }
 };
-constexpr int kNumPanelCfgs = 4;
+constexpr int kNumPanelCfgs = 5;
 extern const PanelCfg kPanelCfgs[kNumPanelCfgs];
 // LDS bytes of a panel kernel launch whose channel groups' tables and panels
 // take `stride` bytes each

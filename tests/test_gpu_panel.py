@@ -16,7 +16,7 @@ from test_gpu_parity import KINDS, _case, check, say
 pytestmark = pytest.mark.gpu
 
 T = 1  # SL_LAYOUT_T16X32
-SHAPES = ["6,2,8,2", "4,2,8,2", "2,2,8,4", "2,4,4,2"]
+SHAPES = ["6,2,12,2", "6,2,8,2", "4,2,8,2", "2,2,8,4", "2,4,4,2"]
 
 # (m, n, k, density): k a multiple of 16 so that row-major rows qualify too
 CASES = [
@@ -113,8 +113,9 @@ def test_default_path_choice(hip, monkeypatch):
     import workloads as wk
     monkeypatch.delenv("SL_PATH", raising=False)
     monkeypatch.delenv("SL_PTILE", raising=False)
-    for (n, k, m, s, want) in [(3072, 768, 4096, 0.9, "panel 6,2,8,2"), (3072, 768, 4096, 0.8, "panel 6,2,8,2"),
-                               (3072, 768, 16384, 0.8, "panel 6,2,8,2"), (2304, 768, 384, 0.8, "panel"),
+    for (n, k, m, s, want) in [(3072, 768, 4096, 0.9, "panel 6,2,12,2"), (3072, 768, 4096, 0.8, "panel 6,2,12,2"),
+                               (3072, 768, 16384, 0.8, "panel 6,2,12,2"), (2304, 768, 4096, 0.8, "panel 6,2,12,2"),
+                               (2304, 768, 384, 0.8, "panel"),
                                (768, 3072, 4096, 0.9, "direct"), (768, 768, 4096, 0.8, "direct"),
                                (768, 768, 128, 0.9, "split"), (3072, 768, 128, 0.8, "split"),
                                (768, 3072, 384, 0.8, "split"), (768, 768, 1024, 0.8, "direct")]:
