@@ -983,6 +983,31 @@ static DirectCfg choose_direct_cfg(int64_t m, const sl_packed_weight *w)
 // of at most this many 128-feature windows (K <= 1024).
 constexpr int32_t kPanelMaxWin = 8;
 
+// Whether the work items of the kernel that runs where the weight-stationary
+// one does not (direct, else staged) make one round of the CUs that keeps at
+// least 80 % of them busy. Over short reductions that kernel wins only
+// there: a second round costs a whole item's time again, where the
+// weight-stationary kernel reuses its panel.
+static bool one_full_round(bool direct, int64_t m, const sl_packed_weight *w)
+{
+    int dev = 0, n_cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n_cu < 1)
+        return true;
+    int64_t tm, nt;
+    if (direct) {
+        const DirectCfg c = choose_direct_cfg(m, w);
+        tm = c.tm();
+        nt = c.nt;
+    } else {
+        const TileCfg c = choose_cfg(m, w);
+        tm = c.tm();
+        nt = c.nt();
+    }
+    const int64_t items = (m + tm - 1) / tm * ((w->tiles.n_tiles + nt - 1) / nt);
+    return items <= n_cu && items * 5 >= (int64_t)n_cu * 4;
+}
+
 // Weight-stationary shape for a launch of a.m tokens: the compiled shapes
 // whose largest panel fits in LDS are scored by the bytes their workgroups
 // read (token rows once per channel group, the panel once per workgroup)
@@ -1129,10 +1154,11 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int32_t x_la
         const bool vec = xt || ((w->k_in % 16 == 0) && ((reinterpret_cast<uintptr_t>(a.x) & 15) == 0));
         // Aligned or block-layout rows: the weight-stationary kernel where it
         // pays -- a short reduction (at most kPanelMaxWin windows), and either
-        // a widening layer (N > K: many channel groups share each token row)
-        // or slices of at least four token groups per wave (the panel filled
-        // once is used for many tokens) -- with the shape the cost model
-        // picks; else the direct-operand kernel (block-layout input, or
+        // a widening layer (N > K: many channel groups share each token row),
+        // slices of at least four token groups per wave (the panel filled
+        // once is used for many tokens), or unless the other kernel's work
+        // items make one round of the CUs that keeps most of them busy --
+        // with the shape the cost model picks; else the direct-operand kernel (block-layout input, or
         // block-layout output from aligned rows) or the staged kernel
         // (row-major input and output). SL_PATH=panel|direct|staged forces a
         // kernel (tests, tuning; panel falls back when no panel fits).
@@ -1162,11 +1188,14 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int32_t x_la
         }
         const bool force_panel = strcmp(path, "panel") == 0;
         const bool auto_path = !*path;
+        const bool direct = (xt || (yt && vec) || (vec && strcmp(path, "direct") == 0)) &&
+                            !(strcmp(path, "staged") == 0 && !xt && !yt);
         if (vec && (force_panel || (auto_path && ti.n_win <= kPanelMaxWin))) {
             PanelCfg pc{};
             size_t lds = 0;
             sl_status pst = choose_panel_cfg(a, w, run_kind, yt, &pc, &lds);
-            if (pst == SL_OK && !force_panel && !(w->n_out > w->k_in || a.slice_groups >= 4 * pc.nwv))
+            if (pst == SL_OK && !force_panel &&
+                !(w->n_out > w->k_in || a.slice_groups >= 4 * pc.nwv || !one_full_round(direct, a.m, w)))
                 pst = SL_ERR_UNSUPPORTED;
             if (pst == SL_OK) {
                 pst = launch_panel(a, run_kind == SL_EPI_I8_GELU ? &ga : nullptr, run_kind, pc, xt, yt, lds, s);
@@ -1177,8 +1206,6 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int32_t x_la
             }
             if (pst != SL_ERR_UNSUPPORTED) return pst;
         }
-        const bool direct = (xt || (yt && vec) || (vec && strcmp(path, "direct") == 0)) &&
-                            !(strcmp(path, "staged") == 0 && !xt && !yt);
         TileCfg cfg{};
         DirectCfg dcfg{};
         int nt, tm;

@@ -106,9 +106,12 @@ def test_default_path_choice(hip, monkeypatch):
     """Without SL_PATH few tokens (at most 1280 work items of 16 tokens x 32
     channels) go to the split-reduction kernel; beyond that the
     weight-stationary kernel runs for short reductions (K <= 1024) of
-    widening layers (DistilBERT QKV and FFN1) or of long token slices, and
-    the direct kernel elsewhere: FFN2 (K = 3072) and the square
-    attention-output layer."""
+    widening layers (DistilBERT QKV and FFN1), of long token slices, or
+    unless the direct kernel's work items make one round of the CUs that
+    keeps most of them busy (not so for the square 768 layer at 1024 or
+    8192 tokens, or 1024x1024 at 4096); the direct kernel elsewhere: FFN2
+    (K = 3072) and the square attention-output layer at 2048 and 4096
+    tokens."""
     import torch
     import workloads as wk
     monkeypatch.delenv("SL_PATH", raising=False)
@@ -118,7 +121,9 @@ def test_default_path_choice(hip, monkeypatch):
                                (2304, 768, 384, 0.8, "panel"),
                                (768, 3072, 4096, 0.9, "direct"), (768, 768, 4096, 0.8, "direct"),
                                (768, 768, 128, 0.9, "split"), (3072, 768, 128, 0.8, "split"),
-                               (768, 3072, 384, 0.8, "split"), (768, 768, 1024, 0.8, "direct")]:
+                               (768, 3072, 384, 0.8, "split"), (768, 768, 1024, 0.8, "panel"),
+                               (768, 768, 2048, 0.8, "direct"), (1024, 1024, 4096, 0.8, "panel"),
+                               (768, 768, 8192, 0.8, "panel")]:
         wd = wk.make_weight(n, k, s, seed=3)
         x = wk.make_x(m, k, seed=3)
         pw = hip.PackedWeight.pack(wd["w"], wd["sw"], wd["b"])
