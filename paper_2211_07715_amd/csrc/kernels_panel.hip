@@ -265,10 +265,36 @@ __device__ __forceinline__ void panel_body(const LinearArgs &a, const GeluArg *e
                     float s0[4], b0[4], s1[4], b1[4];
                     scales(c, s0, b0);
                     scales(c + 1, s1, b1);
+                    // the GELU kind's table reads for the pair's ST subtiles
+                    // are issued together, so that their LDS latency (and
+                    // bank conflicts: the cells are data-dependent) is met
+                    // once per pair rather than once per two outputs
+                    [[maybe_unused]] float gy[ST][2][4];
+                    [[maybe_unused]] u32x2 gcell[ST][2][4];
+                    if constexpr (KIND == SL_EPI_I8_GELU) {
+                        uint32_t ad[ST][2][4];
+#pragma unroll
+                        for (int st = 0; st < ST; ++st) {
+                            gelu_cells(acc[c][st], s0, b0, tab, hinv, eoff, cmax, gy[st][0], ad[st][0]);
+                            gelu_cells(acc[c + 1][st], s1, b1, tab, hinv, eoff, cmax, gy[st][1], ad[st][1]);
+                        }
+#pragma unroll
+                        for (int st = 0; st < ST; ++st)
+#pragma unroll
+                            for (int h = 0; h < 2; ++h)
+#pragma unroll
+                                for (int r = 0; r < 4; ++r) gcell[st][h][r] = lds_read_u2(ad[st][h][r]);
+                    }
 #pragma unroll
                     for (int st = 0; st < ST; ++st) {
-                        const uint32_t v0 = epilogue_value<KIND>(a, acc[c][st], s0, b0, tab, hinv, eoff, cmax);
-                        const uint32_t v1 = epilogue_value<KIND>(a, acc[c + 1][st], s1, b1, tab, hinv, eoff, cmax);
+                        uint32_t v0, v1;
+                        if constexpr (KIND == SL_EPI_I8_GELU) {
+                            v0 = gelu_codes(gy[st][0], gcell[st][0]);
+                            v1 = gelu_codes(gy[st][1], gcell[st][1]);
+                        } else {
+                            v0 = epilogue_value<KIND>(a, acc[c][st], s0, b0, tab, hinv, eoff, cmax);
+                            v1 = epilogue_value<KIND>(a, acc[c + 1][st], s1, b1, tab, hinv, eoff, cmax);
+                        }
                         // (a wave's LDS operations take effect in order: the
                         // previous block's read is done before these writes)
                         tr[wi] = v0;

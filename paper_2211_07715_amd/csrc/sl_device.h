@@ -163,6 +163,47 @@ __device__ __forceinline__ u32x2 lds_read_u2(uint32_t addr)
     return *(const __attribute__((address_space(3))) u32x2 *)(uintptr_t)addr;
 }
 
+// The int8 GELU step-table epilogue in two halves, so that a caller can
+// issue the table reads of many accumulator groups before it needs any:
+// gelu_cells computes y = acc s + b (two fp32 roundings, as the definition)
+// and the LDS address of y's cell for 4 accumulators; gelu_codes packs the
+// 4 codes once the cells (threshold, then the two codes) have been read.
+__device__ __forceinline__ void gelu_cells(const i32x4 acc, const float s[4], const float b[4], const GeluCell *tab,
+                                           float hinv, float off, float cmax, float (&y)[4], uint32_t (&ad)[4])
+{
+#pragma clang fp contract(off)
+    // (read through readfirstlane: a uniform register operand of the
+    // shift-and-add, not a constant folded into two instructions)
+    const uint32_t tab_adj = (uint32_t)__builtin_amdgcn_readfirstlane(
+        (int)((uint32_t)(uintptr_t)(const __attribute__((address_space(3))) GeluCell *)tab -
+              (__float_as_uint(kGeluBase) << 3)));
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        float v = (float)acc[r] * s[r];
+        v = v + b[r];
+        y[r] = v;
+        // the bits of c are those of kGeluBase plus the cell index (see
+        // kGeluBase), so one shift-and-add with tab_adj = (LDS address of
+        // the table) - 8 * bits(kGeluBase), modulo 2^32, gives the cell's
+        // address
+        const float c = __builtin_amdgcn_fmed3f(__builtin_fmaf(v, hinv, off), kGeluBase, cmax);
+        ad[r] = (__float_as_uint(c) << 3) + tab_adj;
+    }
+}
+__device__ __forceinline__ uint32_t gelu_codes(const float (&y)[4], const u32x2 (&cell)[4])
+{
+    // byte selectors of the permute that writes code r into byte r of the
+    // packed word: earlier bytes kept (4 + i), byte r taken from the cell's
+    // codes (0: q_lo, 1: q_hi), later bytes zero (0x0c)
+    constexpr uint32_t kSelLo[4] = {0x0c0c0c00u, 0x0c0c0004u, 0x0c000504u, 0x00060504u};
+    constexpr uint32_t kSelHi[4] = {0x0c0c0c01u, 0x0c0c0104u, 0x0c010504u, 0x01060504u};
+    uint32_t packed = 0;
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+        packed = __builtin_amdgcn_perm(packed, cell[r].y, y[r] >= __uint_as_float(cell[r].x) ? kSelHi[r] : kSelLo[r]);
+    return packed;
+}
+
 // Epilogue of one accumulator group: s = input scale x weight scales, b =
 // biases of the 4 channels; tab, hinv, off, cmax (= kGeluBase + cells - 1):
 // the GELU step table.
@@ -176,30 +217,13 @@ __device__ __forceinline__ typename EpiOut<KIND>::T epilogue_value_s(float inv_s
     if constexpr (KIND == SL_EPI_ACC_I32) {
         return acc;
     } else if constexpr (KIND == SL_EPI_I8_GELU) {
-        // byte selectors of the permute that writes code r into byte r of
-        // the packed word: earlier bytes kept (4 + i), byte r taken from the
-        // cell's codes (0: q_lo, 1: q_hi), later bytes zero (0x0c)
-        constexpr uint32_t kSelLo[4] = {0x0c0c0c00u, 0x0c0c0004u, 0x0c000504u, 0x00060504u};
-        constexpr uint32_t kSelHi[4] = {0x0c0c0c01u, 0x0c0c0104u, 0x0c010504u, 0x01060504u};
-        // (read through readfirstlane: a uniform register operand of the
-        // shift-and-add, not a constant folded into two instructions)
-        const uint32_t tab_adj = (uint32_t)__builtin_amdgcn_readfirstlane(
-            (int)((uint32_t)(uintptr_t)(const __attribute__((address_space(3))) GeluCell *)tab -
-                  (__float_as_uint(kGeluBase) << 3)));
-        uint32_t packed = 0;
+        float y[4];
+        uint32_t ad[4];
+        gelu_cells(acc, s, b, tab, hinv, off, cmax, y, ad);
+        u32x2 cell[4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            float y = (float)acc[r] * s[r];
-            y = y + b[r];
-            const float c = __builtin_amdgcn_fmed3f(__builtin_fmaf(y, hinv, off), kGeluBase, cmax);
-            // one 8-byte read: threshold, then the two codes. The bits of c
-            // are those of kGeluBase plus the cell index (see kGeluBase), so
-            // one shift-and-add with tab_adj = (LDS address of the table) -
-            // 8 * bits(kGeluBase), modulo 2^32, gives the cell's address.
-            const u32x2 cell = lds_read_u2((__float_as_uint(c) << 3) + tab_adj);
-            packed = __builtin_amdgcn_perm(packed, cell.y, y >= __uint_as_float(cell.x) ? kSelHi[r] : kSelLo[r]);
-        }
-        return packed;
+        for (int r = 0; r < 4; ++r) cell[r] = lds_read_u2(ad[r]);
+        return gelu_codes(y, cell);
     } else {
         float g[4];
 #pragma unroll
