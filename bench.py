@@ -246,10 +246,12 @@ def time_instep(torch, r, steps, stream):
         ev[i][n_k].record(stream)
     torch.cuda.synchronize()
     v = np.array([[ev[i][j].elapsed_time(ev[i][j + 1]) * 1e3 for j in range(n_k)] for i in range(steps)])
+    # whole steps, first kernel's event to the last one's
+    tot = np.array([ev[i][0].elapsed_time(ev[i][n_k]) * 1e3 for i in range(steps)])
     # mean over the central 90 % of the steps (a rare stall of the device
     # queue, milliseconds long, would otherwise dominate the average)
     lo, hi = np.percentile(v, 5, axis=0), np.percentile(v, 95, axis=0)
-    return np.array([v[(v[:, j] >= lo[j]) & (v[:, j] <= hi[j]), j].mean() for j in range(n_k)])
+    return np.array([v[(v[:, j] >= lo[j]) & (v[:, j] <= hi[j]), j].mean() for j in range(n_k)]), tot
 
 
 def time_legs(torch, r):
@@ -566,7 +568,7 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     ms_warm = time_steps(torch, r, args.steps, stream, rotate=False)
-    instep = time_instep(torch, r, args.steps, stream)
+    instep, step_tot = time_instep(torch, r, args.steps, stream)
     legs = time_legs(torch, r)
 
     peaks = None if args.no_extra else measure_peaks(torch, dev)
@@ -636,6 +638,11 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": round(ms_cold, 5),
         "ms_per_step_warm": round(ms_warm, 5),
+        # per-step durations from the in-step pass (an event at every step
+        # boundary and between kernels, so slightly above ms_per_step)
+        "step_us_events": {"mean": round(float(step_tot.mean()), 2), "median": round(float(np.median(step_tot)), 2),
+                           "p5": round(float(np.percentile(step_tot, 5)), 2),
+                           "p95": round(float(np.percentile(step_tot, 95)), 2)},
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
