@@ -238,8 +238,9 @@ const char *sl_last_path(void);
 
 /*
  * Kernel selection overrides, for tuning and tests: SL_PATH (split, panel,
- * direct, staged) and the tile shapes SL_TILE / SL_DTILE / SL_PTILE are
- * read from the environment once, at the first run; sl_reload_env() reads
+ * direct, staged), the tile shapes SL_TILE / SL_DTILE / SL_PTILE and the
+ * weight-stationary kernel's token-slice count SL_PSLICES are read from
+ * the environment once, at the first run; sl_reload_env() reads
  * them again (call it after changing them, with no run in flight on any
  * thread).
  */

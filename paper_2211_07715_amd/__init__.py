@@ -45,7 +45,7 @@ EXPORTS = ("sparse_linear_pack", "sparse_linear_pack_host", "sparse_linear_run",
            "sl_abi_version", "sl_last_path", "sl_reload_env", "sl_gelu_table_codes")
 
 # kernel-selection overrides the library reads from the environment
-ENV_KEYS = ("SL_PATH", "SL_TILE", "SL_DTILE", "SL_PTILE")
+ENV_KEYS = ("SL_PATH", "SL_TILE", "SL_DTILE", "SL_PTILE", "SL_PSLICES")
 _env_seen: Optional[tuple] = None
 
 _lib: Optional[ctypes.CDLL] = None

@@ -57,6 +57,7 @@ void reload_env()
     parse_ints(getenv("SL_TILE"), e.tile, 5);
     parse_ints(getenv("SL_DTILE"), e.dtile, 4);
     parse_ints(getenv("SL_PTILE"), e.ptile, 4);
+    parse_ints(getenv("SL_PSLICES"), &e.pslices, 1);
     g_env = e;
 }
 

@@ -1012,8 +1012,10 @@ static bool one_full_round(bool direct, int64_t m, const sl_packed_weight *w)
 // whose largest panel fits in LDS are scored by the bytes their workgroups
 // read (token rows once per channel group, the panel once per workgroup)
 // spread over the CUs they keep busy, with a small preference for more
-// resident waves a SIMD; SL_PTILE="nt,st,nwv,r" overrides. Fills a's
-// channel-group and slice fields; SL_ERR_UNSUPPORTED when no panel fits.
+// resident waves a SIMD; SL_PTILE="nt,st,nwv,r" overrides the shape and
+// SL_PSLICES=n the number of token slices (tests: many token groups a wave
+// at small sizes). Fills a's channel-group and slice fields;
+// SL_ERR_UNSUPPORTED when no panel fits.
 static sl_status choose_panel_cfg(LinearArgs &a, const sl_packed_weight *w, int32_t run_kind, bool yt, PanelCfg *out,
                                   size_t *lds_out)
 {
@@ -1060,7 +1062,7 @@ static sl_status choose_panel_cfg(LinearArgs &a, const sl_packed_weight *w, int3
         // workgroup a CU (fewer panel fills, more token groups a wave),
         // whichever scores better
         for (int64_t want : {res / n_cg, (int64_t)n_cu / n_cg}) {
-            want = std::max<int64_t>(1, want);
+            want = std::max<int64_t>(1, env_cfg().pslices > 0 ? env_cfg().pslices : want);
             const int64_t sg = std::max<int64_t>(1, (groups + want - 1) / want);
             const int64_t n_sl = (groups + sg - 1) / sg;
             const int64_t nwg = n_cg * n_sl;

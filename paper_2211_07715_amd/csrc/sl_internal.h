@@ -158,6 +158,7 @@ struct EnvCfg {
     int tile[5];    // SL_TILE "st,ct,wm,wn,d"; tile[0] == 0: unset
     int dtile[4];   // SL_DTILE "st,nt,wm,d"
     int ptile[4];   // SL_PTILE "nt,st,nwv,r"
+    int pslices;    // SL_PSLICES: token slices of the weight-stationary kernel (0: its cost model picks)
 };
 const EnvCfg &env_cfg();
 void reload_env();
