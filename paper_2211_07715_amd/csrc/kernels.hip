@@ -1155,12 +1155,13 @@ sl_status launch_linear(const sl_packed_weight *w, const int8_t *x, int32_t x_la
         a.m = std::min(chunk, m - t0);
         const bool vec = xt || ((w->k_in % 16 == 0) && ((reinterpret_cast<uintptr_t>(a.x) & 15) == 0));
         // Aligned or block-layout rows: the weight-stationary kernel where it
-        // pays -- a short reduction (at most kPanelMaxWin windows), and either
-        // a widening layer (N > K: many channel groups share each token row),
-        // slices of at least four token groups per wave (the panel filled
-        // once is used for many tokens), or unless the other kernel's work
-        // items make one round of the CUs that keeps most of them busy --
-        // with the shape the cost model picks; else the direct-operand kernel (block-layout input, or
+        // pays -- a short reduction (at most kPanelMaxWin windows), and a
+        // widening layer (N > K: many channel groups share each token row),
+        // or slices of at least four token groups per wave (the panel filled
+        // once is used for many tokens), or work items of the other kernel
+        // that would not make one round of the CUs keeping most of them
+        // busy -- with the shape the cost model picks; else the
+        // direct-operand kernel (block-layout input, or
         // block-layout output from aligned rows) or the staged kernel
         // (row-major input and output). SL_PATH=panel|direct|staged forces a
         // kernel (tests, tuning; panel falls back when no panel fits).
